@@ -1,0 +1,113 @@
+"""Seeded synthetic workloads for the multi-head LM loss.
+
+This module only draws random inputs (hidden states, heads, labels) with
+the shapes and value distributions of the benchmark workloads; it holds
+none of the loss arithmetic, so the GPU path and the CPU oracle can both be
+fed from it.
+
+The paper trains on FineWeb-Edu with the SmolLM2 tokenizer (V = 49,152;
+section 3, "Experimental Setup") and packs sequences to 2,048 tokens. That
+corpus is not available here: uniform random labels and Gaussian hidden
+states / heads of the same shapes stand in for it. The value distributions
+change the numbers, not the cost of the computation.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Optional, Sequence, Tuple
+
+import torch
+
+IGNORE_INDEX = -100
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    """Shape and distribution of one synthetic problem.
+
+    ``w_std`` is the standard deviation of every head entry; ``None`` means
+    ``1 / sqrt(d_i)`` per sub-model. ``w_scale`` multiplies the heads after
+    drawing (used to make logits peaky). ``ignore_frac`` is the Bernoulli
+    probability that a label is replaced by ``IGNORE_INDEX``.
+    """
+
+    name: str
+    M: int
+    T: int
+    dims: Tuple[int, ...]
+    V: int
+    dtype: str = "bf16"          # "bf16" or "f32": the dtype of h_i and W_i
+    alpha: float = 1.0
+    tau: float = 1.0
+    w_std: Optional[float] = 0.02
+    w_scale: float = 1.0
+    ignore_frac: float = 0.0
+    seed: int = 0
+    batch: int = 1
+    seq: int = 0
+
+    def replace(self, **kw) -> "Workload":
+        return dataclasses.replace(self, **kw)
+
+    @property
+    def torch_dtype(self):
+        return torch.bfloat16 if self.dtype == "bf16" else torch.float32
+
+    def algorithmic_flops(self) -> float:
+        """Dense work of one forward + backward pass: three GEMMs of 2*T*V*d_i."""
+        return 6.0 * self.T * self.V * float(sum(self.dims))
+
+
+# The five benchmark workloads plus the head shape of the paper's 3B suite
+# (Table 1: widths 1024 / 2304 / 4352, V = 49,152; alpha_d = 0.3 from
+# section 3, "Experimental Setup").
+WORKLOADS = {
+    "c1_small_f32": Workload("c1_small_f32", 2, 256, (128, 256), 4096, "f32",
+                             alpha=1.0, tau=1.0, w_std=None, seed=1001, batch=1, seq=256),
+    "c2_m3_v50k": Workload("c2_m3_v50k", 3, 4096, (1024, 2048, 3072), 50304, "bf16",
+                           alpha=1.0, tau=1.0, seed=1002, batch=2, seq=2048),
+    "c3_m3_v128k_tau2": Workload("c3_m3_v128k_tau2", 3, 8192, (1024, 2048, 3072), 128256,
+                                 "bf16", alpha=0.5, tau=2.0, seed=1003, batch=4, seq=2048),
+    "c4_m4_v128k_peaky": Workload("c4_m4_v128k_peaky", 4, 16384, (512, 1024, 2048, 4096),
+                                  128256, "bf16", alpha=1.0, tau=1.0, w_scale=5.0,
+                                  ignore_frac=0.1, seed=1004, batch=8, seq=2048),
+    "c5_m3_v262k_long": Workload("c5_m3_v262k_long", 3, 32768, (1536, 3072, 4608), 262144,
+                                 "bf16", alpha=1.0, tau=1.0, seed=1005, batch=4, seq=8192),
+    "paper3b_heads": Workload("paper3b_heads", 3, 4096, (1024, 2304, 4352), 49152, "bf16",
+                              alpha=0.3, tau=1.0, seed=1006, batch=2, seq=2048),
+}
+
+HEADLINE = "c2_m3_v50k"
+
+
+def make_inputs(wl: Workload, device="cpu", seed: Optional[int] = None):
+    """Draw ``(h_list, W_list, labels)`` for a workload on ``device``.
+
+    Draw order from one generator: h_0..h_{M-1}, W_0..W_{M-1}, labels,
+    ignore mask. Values are drawn in float32 and rounded to the workload dtype.
+    """
+    g = torch.Generator(device=device)
+    g.manual_seed(wl.seed if seed is None else seed)
+    dt = wl.torch_dtype
+    hs = []
+    for d in wl.dims:
+        hs.append(torch.randn(wl.T, d, generator=g, device=device, dtype=torch.float32).to(dt))
+    Ws = []
+    for d in wl.dims:
+        std = (1.0 / math.sqrt(d)) if wl.w_std is None else wl.w_std
+        w = torch.randn(wl.V, d, generator=g, device=device, dtype=torch.float32)
+        w.mul_(std * wl.w_scale)
+        Ws.append(w.to(dt))
+        del w
+    labels = torch.randint(0, wl.V, (wl.T,), generator=g, device=device, dtype=torch.int64)
+    if wl.ignore_frac > 0:
+        drop = torch.rand(wl.T, generator=g, device=device) < wl.ignore_frac
+        labels = torch.where(drop, torch.full_like(labels, IGNORE_INDEX), labels)
+    return hs, Ws, labels
+
+
+def custom(M: int, T: int, dims: Sequence[int], V: int, dtype="bf16", **kw) -> Workload:
+    """A workload of arbitrary shape (for parity tests below full size)."""
+    return Workload(kw.pop("name", f"custom_m{M}_t{T}_v{V}"), M, T, tuple(dims), V, dtype, **kw)
