@@ -1,0 +1,207 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused multi-sub-model LM head + CE + KL, forward + backward, on one MI355X.
+
+One step = mls_distill_fwd + mls_distill_bwd over one batch of synthetic input that is
+already resident in HBM: every sub-model's logits, online log-sum-exp, cross-entropy,
+teacher-to-student KL, and the gradients grad_h_i and grad_W_i with the coefficients of
+eq. (3). Prints one JSON line (see README of the build for the fields).
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "fused LM-head+CE+KL fwd+bwd tokens/s (M=3, V=50304); % of bf16 MFMA peak"
+PEAK_FLOPS = {"bf16": 2.5e15, "f32": 157.3e12}  # MI355X dense MFMA peaks
+HBM_PEAK = 8.0e12
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample rows (0 = auto)")
+    ap.add_argument("--vocab-chunk", type=int, default=0)
+    return ap.parse_args()
+
+
+def cpu_baseline(wl, h, W, y, g_ce, g_kl, rows_req):
+    """Times the float64 CPU oracle (forward + backward) on a sample of rows."""
+    import numpy as np
+    import oracle
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()
+                       if p.get("user_api") == "blas"] or [os.cpu_count() or 1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    Wn = [x.float().cpu().numpy() for x in W]
+    yn_all = y.cpu().numpy()
+
+    def run(nrows):
+        hn = [x[:nrows].float().cpu().numpy() for x in h]
+        yn = yn_all[:nrows]
+        t0 = time.perf_counter()
+        oracle.forward(hn, Wn, yn, tau=wl.tau)
+        oracle.backward(hn, Wn, yn, g_ce, g_kl, tau=wl.tau)
+        return time.perf_counter() - t0
+
+    if rows_req > 0:
+        rows = rows_req
+    else:
+        probe = 16
+        tp = run(probe)
+        rows = int(min(wl.T, max(probe, probe * 15.0 / max(tp, 1e-3))))
+        rows = max(16, rows // 16 * 16)
+        log(f"oracle probe: {probe} rows in {tp:.2f}s -> sample {rows} rows")
+    dt = run(rows)
+    return {
+        "value": rows / dt,
+        "unit": "tokens/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"float64 numpy oracle, forward + backward on the first {rows} of {wl.T} tokens "
+                  f"at full V={wl.V} and widths {list(wl.dims)}; {dt:.1f} s",
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not part "
+                                   "of it (see the sharding design note)", "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+    from paper_2608_09703_amd import binding as B
+    from paper_2608_09703_amd import distill as D
+    from paper_2608_09703_amd import workloads as WL
+
+    name = args.workload or WL.HEADLINE
+    wl = WL.WORKLOADS[name]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(f"workload {name}: M={wl.M} T={wl.T} dims={wl.dims} V={wl.V} {wl.dtype} "
+        f"alpha={wl.alpha} tau={wl.tau}")
+    h, W, y = WL.make_inputs(wl, device=dev)
+    p = D.make_problem(h, W, y, tau=wl.tau, alpha=wl.alpha, vocab_chunk=args.vocab_chunk)
+    buf = D.Buffers(p, dev)
+    g_ce, g_kl = D.coefficients(wl.M, alpha=wl.alpha, tau=wl.tau)
+    gce = torch.tensor(g_ce, dtype=torch.float32, device=dev)
+    gkl = torch.tensor(g_kl, dtype=torch.float32, device=dev)
+    gh = [torch.empty(x.shape, dtype=torch.float32, device=dev) for x in h]
+    gW = [torch.empty(x.shape, dtype=torch.float32, device=dev) for x in W]
+    stream = torch.cuda.current_stream(dev)
+    sh = stream.cuda_stream
+    ws_ptr, ws_n = buf.workspace.data_ptr(), buf.workspace.numel()
+    st_ptr = buf.stats.data_ptr()
+    gh_p = [x.data_ptr() for x in gh]
+    gW_p = [x.data_ptr() for x in gW]
+
+    def step():
+        B.distill_fwd(p, st_ptr, buf.ce.data_ptr(), buf.kl.data_ptr(), buf.entropy.data_ptr(),
+                      ws_ptr, ws_n, sh)
+        B.distill_bwd(p, st_ptr, gce.data_ptr(), gkl.data_ptr(), gh_p, gW_p, ws_ptr, ws_n, sh)
+
+    log(f"workspace {ws_n / 2**20:.0f} MiB, stats {buf.stats.numel() / 2**20:.1f} MiB")
+    for k in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} steps done")
+
+    B.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for k in range(args.steps):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    B.profile_enable(False)
+    prof = B.profile_report()
+    ms_total = t0.elapsed_time(t1)
+    ms_step = ms_total / args.steps
+    tokens_per_s = wl.T / (ms_step / 1e3)
+    flops_step = wl.algorithmic_flops()
+    peak = PEAK_FLOPS[wl.dtype]
+    pct = flops_step / (ms_step / 1e3) / peak * 100.0
+    log(f"{args.steps} steps: {ms_step:.3f} ms/step, {tokens_per_s:,.0f} tokens/s, "
+        f"{pct:.1f}% of {wl.dtype} MFMA peak (algorithmic 6*T*V*sum(d))")
+
+    # per-kernel times from the library's event timer over the timed region
+    kernels = {}
+    for kname, (launches, tot) in prof.items():
+        kernels[kname] = {"launches_per_step": launches / args.steps,
+                          "ms_per_step": tot / args.steps,
+                          "avg_launch_ms": tot / launches}
+        log(f"  {kname:14s} {launches / args.steps:5.1f} launches/step "
+            f"{tot / args.steps:8.3f} ms/step  avg {tot / launches:8.4f} ms")
+    # each of the four MFMA kernels performs one 2*T*V*sum(d) contraction per step
+    dense = {"fused_fwd", "fused_bwd", "gemm_grad_W", "gemm_grad_h"}
+    dom = max((k for k in kernels if k in dense), key=lambda k: kernels[k]["ms_per_step"])
+    per_step = 2.0 * wl.T * wl.V * sum(wl.dims)
+    per_launch = per_step / kernels[dom]["launches_per_step"]
+    achieved = per_launch / (kernels[dom]["avg_launch_ms"] / 1e3)
+    roofline = {
+        "bound": "mfma",
+        "kernel": dom,
+        "achieved": achieved / 1e12,
+        "peak": peak / 1e12,
+        "unit": "TFLOP/s",
+        "frac": achieved / peak,
+        "traffic": None,
+    }
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a sample of rows")
+        cpu = cpu_baseline(wl, h, W, y, g_ce, g_kl, args.cpu_rows)
+        log(f"oracle: {cpu['value']:.2f} tokens/s on {cpu['cores']} threads")
+
+    out = {
+        "metric": METRIC,
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded Gaussian hidden states and heads, uniform labels)",
+        "config": {"workload": name, "M": wl.M, "T": wl.T, "batch": wl.batch, "seq": wl.seq,
+                   "widths": list(wl.dims), "V": wl.V, "alpha": wl.alpha, "tau": wl.tau,
+                   "ignore_frac": wl.ignore_frac, "parallelism": "single GPU"},
+        "pct_of_bf16_peak": pct if wl.dtype == "bf16" else None,
+        "algorithmic_tflop_per_step": flops_step / 1e12,
+        "roofline": roofline,
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

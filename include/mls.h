@@ -1,0 +1,216 @@
+/*
+ * mls.h - fused multi-sub-model LM head + cross-entropy + distillation on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The operation ("Matryoshka Language Model Suites", section 2, "Method"):
+ * a suite of M nested sub-models, each with its own LM head W_i [V, d_i]
+ * applied to its final hidden states h_i [T, d_i] (paragraphs "Modeling" and
+ * "Inter-model Junction"); every sub-model takes next-token cross-entropy;
+ * every sub-model except the teacher s (the largest one) adds a distillation
+ * term from the teacher's stop-gradient softmax (eq. (2)); the sub-model
+ * losses are combined convexly (eq. (3)) and summed.
+ *
+ * The library computes, for every sub-model i and valid token t
+ * (label y_t != ignore_index):
+ *   l_i[t]     = W_i h_i[t]                          logits, never stored
+ *   CE_i       = mean_t ( logsumexp(l_i[t]) - l_i[t, y_t] )
+ *   KL_i       = mean_t KL( q[t] || softmax(l_i[t] / tau) ),  KL_s = 0,
+ *                q[t] = softmax(l_s[t] / tau)
+ *   H          = mean_t entropy(q[t])
+ * eq. (2) at temperature tau is KL_i + H. The backward pass is the exact
+ * gradient of J = sum_i g_ce[i] CE_i + g_kl[i] KL_i with q held constant
+ * (stop_grad): with N valid tokens,
+ *   dJ/dl_i[t] = ( g_ce[i] (softmax(l_i) - onehot(y_t))
+ *                + g_kl[i] / tau (softmax(l_i / tau) - q) ) / N,
+ *   grad_h_i = dJ/dl_i  W_i,     grad_W_i = (dJ/dl_i)^T h_i.
+ * eq. (3) with the tau^2 temperature factor is g_ce = (1 - alpha), g_kl =
+ * alpha tau^2 for students and g_ce = 1, g_kl = 0 for the teacher
+ * (mls_coeffs). No [T, V] tensor is ever materialised: the forward keeps
+ * per-row online log-sum-exp statistics, the backward recomputes logits
+ * one vocabulary chunk at a time.
+ *
+ * Conventions
+ *  - Every device buffer is owned and allocated by the caller; the library
+ *    never allocates device memory and keeps no mutable global state. Calls
+ *    on different streams with different workspaces may run concurrently.
+ *  - All device work is enqueued on the given stream (a hipStream_t; NULL is
+ *    the default stream) and is asynchronous: buffers must stay valid until
+ *    the stream reaches the enqueued work.
+ *  - Argument validation is done on the host before any device call; on an
+ *    error nothing is enqueued and the status says why (mls_last_error gives
+ *    the detail, per thread).
+ *  - Row-major layouts. Device pointers to h_i, W_i, grads and workspace must
+ *    be 16-byte aligned, labels 8-byte aligned.
+ */
+#ifndef MLS_H_
+#define MLS_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MLS_MAX_MODELS 8
+
+typedef enum mls_status {
+  MLS_OK = 0,
+  MLS_INVALID_ARG = 1,          /* null pointer, bad size or index, bad tau / alpha, misalignment */
+  MLS_UNSUPPORTED = 2,          /* dtype or width the kernels do not handle */
+  MLS_WORKSPACE_TOO_SMALL = 3,  /* workspace_bytes below what mls_query_sizes reports */
+  MLS_HIP_ERROR = 4             /* a HIP runtime call failed; mls_last_error has its text */
+} mls_status;
+
+typedef enum mls_dtype {
+  MLS_BF16 = 0,  /* bfloat16 h_i and W_i, fp32 accumulation */
+  MLS_F32 = 1    /* float32 h_i and W_i */
+} mls_dtype;
+
+enum mls_mode {
+  MLS_MODE_PAPER = 0,    /* eq. (3): students (1-alpha) CE + alpha tau^2 KL; teacher CE */
+  MLS_MODE_ADDITIVE = 1  /* students CE + alpha tau^2 KL; teacher CE */
+};
+
+enum mls_flags {
+  MLS_ACCUMULATE_GRAD_W = 1u, /* grad_W_i += instead of = */
+  MLS_ACCUMULATE_GRAD_H = 2u  /* grad_h_i += instead of = */
+};
+
+/* Device-side error bits written into the statistics buffer by the forward. */
+enum mls_device_flags {
+  MLS_DEVFLAG_LABEL_RANGE = 1  /* a label outside [0, V) that is not ignore_index;
+                                  such tokens are treated as ignored */
+};
+
+/*
+ * One problem instance. Fields:
+ *   M             number of sub-models, 1..MLS_MAX_MODELS
+ *   teacher       index of the distillation teacher s; -1 selects M-1 (the largest)
+ *   T             number of tokens (batch x sequence, flattened), >= 1
+ *   V             vocabulary size, >= 2
+ *   d[i]          width of sub-model i; a multiple of 8 (bf16) or 4 (f32)
+ *   h[i]          device pointer, [T, d[i]] row-major, in_dtype
+ *   W[i]          device pointer, [V, d[i]] row-major, in_dtype
+ *   labels        device pointer, [T] int64 next-token ids
+ *   ignore_index  label value that removes a token from every loss (usually -100)
+ *   alpha         distillation weight of eq. (3), in [0, 1]; only used when
+ *                 mls_distill_bwd is given no coefficient vectors
+ *   tau           distillation temperature, finite and > 0 (1 = eq. (2) as printed)
+ *   in_dtype      an mls_dtype
+ *   flags         OR of mls_flags
+ *   vocab_chunk   backward vocabulary chunk width (0 = chosen by the library);
+ *                 rounded up to a multiple of 256
+ */
+typedef struct mls_problem {
+  int32_t M;
+  int32_t teacher;
+  int64_t T;
+  int64_t V;
+  int64_t d[MLS_MAX_MODELS];
+  const void* h[MLS_MAX_MODELS];
+  const void* W[MLS_MAX_MODELS];
+  const int64_t* labels;
+  int64_t ignore_index;
+  float alpha;
+  float tau;
+  int32_t in_dtype;
+  uint32_t flags;
+  int64_t vocab_chunk;
+} mls_problem;
+
+/*
+ * Sizes of the two caller-allocated device buffers for problem p.
+ *   workspace_bytes  scratch for one forward or backward call (contents are
+ *                    not kept between calls)
+ *   stats_bytes      per-row statistics the forward writes and the backward
+ *                    reads. Layout (all little-endian, offsets in elements of
+ *                    float32 from the start):
+ *                      lse1[M][T]   log-sum-exp of l_i[t]
+ *                      lset[M][T]   log-sum-exp of l_i[t] / tau
+ *                      ce_row[M][T] per-token CE (0 on ignored tokens)
+ *                      kl_row[M][T] per-token KL (0 on ignored tokens and for the teacher)
+ *                      h_row[T]     per-token teacher entropy (0 on ignored tokens)
+ *                    followed by int32 n_valid and int32 device flags
+ *                    (mls_device_flags).
+ * Pure host function: no device call. Either output pointer may be NULL.
+ */
+mls_status mls_query_sizes(const mls_problem* p, size_t* workspace_bytes, size_t* stats_bytes);
+
+/*
+ * Forward pass. Writes the statistics buffer and the losses:
+ *   ce[M], kl[M]  device float32; kl[teacher] = 0; raw values (no alpha, no tau^2)
+ *   entropy       device float32 [1], mean teacher entropy H (may be NULL)
+ * With no valid token every loss is 0. workspace/workspace_bytes as given by
+ * mls_query_sizes. Asynchronous on stream.
+ */
+mls_status mls_distill_fwd(const mls_problem* p, void* stats, float* ce, float* kl,
+                           float* entropy, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/*
+ * Backward pass: grad_h[i] (device float32 [T, d[i]]) and grad_W[i] (device
+ * float32 [V, d[i]]) of J = sum_i g_ce[i] CE_i + g_kl[i] KL_i, with the
+ * teacher distribution under stop_grad.
+ *   stats        the buffer written by mls_distill_fwd on the same inputs
+ *   g_ce, g_kl   device float32 [M] coefficient vectors (e.g. the upstream
+ *                gradients of ce and kl), read on the device so no host
+ *                synchronisation is needed; if both are NULL the coefficients
+ *                of MLS_MODE_PAPER with p->alpha and p->tau are used. One NULL
+ *                and one non-NULL is an error.
+ *   grad_h       host array of M device pointers; an entry may be NULL to skip
+ *                that gradient. Overwritten unless MLS_ACCUMULATE_GRAD_H.
+ *   grad_W       host array of M device pointers; an entry may be NULL.
+ *                Overwritten unless MLS_ACCUMULATE_GRAD_W.
+ * Asynchronous on stream.
+ */
+mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float* g_ce,
+                           const float* g_kl, float* const* grad_h, float* const* grad_W,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Host helper: loss coefficients of the objective (host arrays of length M).
+ *   mode MLS_MODE_PAPER (eq. (3) summed over sub-models):
+ *     student g_ce = w (1 - alpha), g_kl = w alpha tau^2; teacher g_ce = w, g_kl = 0
+ *   mode MLS_MODE_ADDITIVE:
+ *     student g_ce = w, g_kl = w alpha tau^2; teacher g_ce = w, g_kl = 0
+ * w is the per-sub-model loss weight (appendix G); NULL means all ones.
+ */
+mls_status mls_coeffs(int32_t M, int32_t teacher, float alpha, float tau, int32_t mode,
+                      const float* w, float* g_ce, float* g_kl);
+
+/* Reads the device flags (mls_device_flags) and the valid-token count from a
+ * statistics buffer. Synchronises the stream. Either output may be NULL. */
+mls_status mls_read_stats_header(const mls_problem* p, const void* stats, void* stream,
+                                 int32_t* n_valid, int32_t* device_flags);
+
+/*
+ * Kernel timing, a tracing aid for benchmarks. While enabled (per calling
+ * thread), every kernel the library enqueues from that thread is bracketed
+ * by two hipEvents recorded on the same stream. mls_profile_report waits for
+ * the recorded events, writes at most max_entries aggregated rows (one per
+ * kernel name, in first-launch order) and clears the record.
+ */
+typedef struct mls_kernel_time {
+  char name[32];
+  int32_t launches;
+  double total_ms;
+} mls_kernel_time;
+
+mls_status mls_profile_enable(int32_t enable);
+mls_status mls_profile_report(mls_kernel_time* out, int32_t max_entries, int32_t* n_out);
+
+/* Static text for a status code. */
+const char* mls_status_string(mls_status s);
+
+/* Detail of the last error returned on the calling thread ("" if none). */
+const char* mls_last_error(void);
+
+/* Library version string. */
+const char* mls_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MLS_H_ */

@@ -1,0 +1,203 @@
+"""ctypes binding of ``libmls.so`` (C ABI in ``include/mls.h``).
+
+Argument marshalling only: every step of the loss runs in the library's HIP
+kernels. PyTorch provides device memory and the current stream. The library
+must have been built (``python -m paper_2608_09703_amd.build_lib``); loading
+fails loudly otherwise.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libmls.so")
+
+MAX_MODELS = 8
+
+MLS_OK = 0
+MLS_INVALID_ARG = 1
+MLS_UNSUPPORTED = 2
+MLS_WORKSPACE_TOO_SMALL = 3
+MLS_HIP_ERROR = 4
+
+MLS_BF16 = 0
+MLS_F32 = 1
+
+MLS_MODE_PAPER = 0
+MLS_MODE_ADDITIVE = 1
+
+MLS_ACCUMULATE_GRAD_W = 1
+MLS_ACCUMULATE_GRAD_H = 2
+
+MLS_DEVFLAG_LABEL_RANGE = 1
+
+EXPORTED = (
+    "mls_query_sizes",
+    "mls_distill_fwd",
+    "mls_distill_bwd",
+    "mls_coeffs",
+    "mls_read_stats_header",
+    "mls_status_string",
+    "mls_last_error",
+    "mls_version",
+    "mls_profile_enable",
+    "mls_profile_report",
+)
+
+
+class MlsError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: status {status} ({detail})")
+        self.status = status
+
+
+class KernelTime(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32), ("launches", ctypes.c_int32),
+                ("total_ms", ctypes.c_double)]
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [
+        ("M", ctypes.c_int32),
+        ("teacher", ctypes.c_int32),
+        ("T", ctypes.c_int64),
+        ("V", ctypes.c_int64),
+        ("d", ctypes.c_int64 * MAX_MODELS),
+        ("h", ctypes.c_void_p * MAX_MODELS),
+        ("W", ctypes.c_void_p * MAX_MODELS),
+        ("labels", ctypes.c_void_p),
+        ("ignore_index", ctypes.c_int64),
+        ("alpha", ctypes.c_float),
+        ("tau", ctypes.c_float),
+        ("in_dtype", ctypes.c_int32),
+        ("flags", ctypes.c_uint32),
+        ("vocab_chunk", ctypes.c_int64),
+    ]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with `python -m paper_2608_09703_amd.build_lib`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp = ctypes.c_void_p
+        P = ctypes.POINTER(Problem)
+        fp = ctypes.POINTER(ctypes.c_float)
+        L.mls_query_sizes.argtypes = [P, ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t)]
+        L.mls_distill_fwd.argtypes = [P, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        L.mls_distill_bwd.argtypes = [P, vp, vp, vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp,
+                                      ctypes.c_size_t, vp]
+        L.mls_coeffs.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_float, ctypes.c_float,
+                                 ctypes.c_int32, fp, fp, fp]
+        L.mls_read_stats_header.argtypes = [P, vp, vp, ctypes.POINTER(ctypes.c_int32),
+                                            ctypes.POINTER(ctypes.c_int32)]
+        L.mls_status_string.argtypes = [ctypes.c_int]
+        L.mls_status_string.restype = ctypes.c_char_p
+        L.mls_last_error.argtypes = []
+        L.mls_last_error.restype = ctypes.c_char_p
+        L.mls_version.argtypes = []
+        L.mls_version.restype = ctypes.c_char_p
+        L.mls_profile_enable.argtypes = [ctypes.c_int32]
+        L.mls_profile_report.argtypes = [ctypes.POINTER(KernelTime), ctypes.c_int32,
+                                         ctypes.POINTER(ctypes.c_int32)]
+        for name in ("mls_query_sizes", "mls_distill_fwd", "mls_distill_bwd", "mls_coeffs",
+                     "mls_read_stats_header", "mls_profile_enable", "mls_profile_report"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def check(status: int, where: str):
+    if status != MLS_OK:
+        L = lib()
+        detail = L.mls_last_error().decode() or L.mls_status_string(status).decode()
+        raise MlsError(status, where, detail)
+
+
+def make_problem(M: int, T: int, V: int, dims: Sequence[int], h_ptrs: Sequence[int],
+                 W_ptrs: Sequence[int], labels_ptr: int, *, dtype: int = MLS_BF16,
+                 teacher: int = -1, ignore_index: int = -100, alpha: float = 0.0,
+                 tau: float = 1.0, flags: int = 0, vocab_chunk: int = 0) -> Problem:
+    p = Problem()
+    p.M = M
+    p.teacher = teacher
+    p.T = T
+    p.V = V
+    for i in range(M):
+        p.d[i] = int(dims[i])
+        p.h[i] = h_ptrs[i]
+        p.W[i] = W_ptrs[i]
+    p.labels = labels_ptr
+    p.ignore_index = ignore_index
+    p.alpha = alpha
+    p.tau = tau
+    p.in_dtype = dtype
+    p.flags = flags
+    p.vocab_chunk = vocab_chunk
+    return p
+
+
+def query_sizes(p: Problem):
+    ws = ctypes.c_size_t(0)
+    st = ctypes.c_size_t(0)
+    check(lib().mls_query_sizes(ctypes.byref(p), ctypes.byref(ws), ctypes.byref(st)),
+          "mls_query_sizes")
+    return ws.value, st.value
+
+
+def distill_fwd(p: Problem, stats: int, ce: int, kl: int, entropy: Optional[int], ws: int,
+                ws_bytes: int, stream: int):
+    check(lib().mls_distill_fwd(ctypes.byref(p), stats, ce, kl, entropy, ws, ws_bytes, stream),
+          "mls_distill_fwd")
+
+
+def distill_bwd(p: Problem, stats: int, g_ce: Optional[int], g_kl: Optional[int],
+                grad_h: Sequence[Optional[int]], grad_W: Sequence[Optional[int]], ws: int,
+                ws_bytes: int, stream: int):
+    arr_h = (ctypes.c_void_p * MAX_MODELS)(*[x or None for x in grad_h])
+    arr_W = (ctypes.c_void_p * MAX_MODELS)(*[x or None for x in grad_W])
+    check(lib().mls_distill_bwd(ctypes.byref(p), stats, g_ce, g_kl, arr_h, arr_W, ws, ws_bytes,
+                                stream), "mls_distill_bwd")
+
+
+def coeffs(M: int, teacher: int = -1, alpha: float = 0.0, tau: float = 1.0,
+           mode: int = MLS_MODE_PAPER, w: Optional[Sequence[float]] = None):
+    FA = ctypes.c_float * MAX_MODELS
+    g_ce = FA()
+    g_kl = FA()
+    wa = FA(*w) if w is not None else None
+    check(lib().mls_coeffs(M, teacher, alpha, tau, mode, wa, g_ce, g_kl), "mls_coeffs")
+    return list(g_ce)[:M], list(g_kl)[:M]
+
+
+def read_stats_header(p: Problem, stats: int, stream: int):
+    n = ctypes.c_int32(0)
+    f = ctypes.c_int32(0)
+    check(lib().mls_read_stats_header(ctypes.byref(p), stats, stream, ctypes.byref(n),
+                                      ctypes.byref(f)), "mls_read_stats_header")
+    return n.value, f.value
+
+
+def profile_enable(on: bool = True):
+    check(lib().mls_profile_enable(1 if on else 0), "mls_profile_enable")
+
+
+def profile_report():
+    """{kernel name: (launches, total_ms)} since the last report (waits for the events)."""
+    arr = (KernelTime * 32)()
+    n = ctypes.c_int32(0)
+    check(lib().mls_profile_report(arr, 32, ctypes.byref(n)), "mls_profile_report")
+    return {arr[k].name.decode(): (arr[k].launches, arr[k].total_ms) for k in range(min(n.value, 32))}
+
+
+def version() -> str:
+    return lib().mls_version().decode()

@@ -1,0 +1,569 @@
+// Host side of libmls: argument validation, workspace planning and the launch
+// sequence of the forward and backward passes (C ABI declared in mls.h).
+//
+// Forward:  fused tile kernel (partials) -> label logits -> row merge -> mean.
+// Backward: h_i^T once; then per vocabulary chunk of Vc rows:
+//           W_i[chunk]^T -> fused dlogits tile kernel (slab G, G^T)
+//           -> grad_W_i[chunk] = G^T h_i -> grad_h_i += G W_i[chunk].
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "mls.h"
+#include "mls_launch.h"
+
+namespace {
+
+using namespace mls;
+
+thread_local std::string g_last_error;
+
+// Per-thread kernel timing (mls_profile_enable / mls_profile_report).
+struct ProfRec {
+  const char* name;
+  hipEvent_t start;
+  hipEvent_t stop;
+};
+struct Profiler {
+  bool on = false;
+  std::vector<ProfRec> recs;
+  std::vector<hipEvent_t> pool;
+  hipEvent_t take() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+};
+thread_local Profiler g_prof;
+
+// Brackets one kernel launch with events when profiling is on.
+struct ProfScope {
+  hipStream_t s;
+  ProfRec rec{nullptr, nullptr, nullptr};
+  ProfScope(const char* name, hipStream_t st) : s(st) {
+    if (!g_prof.on) return;
+    rec.name = name;
+    rec.start = g_prof.take();
+    rec.stop = g_prof.take();
+    if (rec.start && rec.stop) hipEventRecord(rec.start, s);
+  }
+  ~ProfScope() {
+    if (!rec.name || !rec.start || !rec.stop) return;
+    hipEventRecord(rec.stop, s);
+    g_prof.recs.push_back(rec);
+  }
+};
+
+mls_status fail(mls_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+mls_status hip_fail(hipError_t e, const char* what) {
+  return fail(MLS_HIP_ERROR, "%s: %s", what, hipGetErrorString(e));
+}
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+constexpr int64_t kSlabTargetBytes = 256ll << 20;  // G and G^T slabs together
+
+struct Plan {
+  int M = 0;
+  int s = 0;
+  bool f32 = false;
+  int es = 2;
+  int64_t T = 0, V = 0;
+  int64_t sumd = 0;
+  int64_t T_pad = 0;
+  int n_tt = 0;
+  int n_vt_fwd = 0;
+  int64_t Vc = 0;
+  int n_chunks = 0;
+  // forward workspace
+  size_t off_partials = 0, off_lab = 0, fwd_bytes = 0;
+  // backward workspace
+  size_t off_slab = 0, off_slabT = 0, off_hT = 0, off_WT = 0, bwd_bytes = 0;
+  size_t ws_bytes = 0;
+  size_t stats_bytes = 0;
+  size_t header_off = 0;
+};
+
+mls_status validate(const mls_problem* p) {
+  if (!p) return fail(MLS_INVALID_ARG, "problem is NULL");
+  if (p->M < 1 || p->M > MLS_MAX_MODELS)
+    return fail(MLS_INVALID_ARG, "M=%d outside [1, %d]", p->M, MLS_MAX_MODELS);
+  if (p->teacher < -1 || p->teacher >= p->M)
+    return fail(MLS_INVALID_ARG, "teacher=%d outside [-1, M)", p->teacher);
+  if (p->T < 1 || p->T > (1ll << 30)) return fail(MLS_INVALID_ARG, "T=%lld out of range", (long long)p->T);
+  if (p->V < 2 || p->V > (1ll << 30)) return fail(MLS_INVALID_ARG, "V=%lld out of range", (long long)p->V);
+  if (p->in_dtype != MLS_BF16 && p->in_dtype != MLS_F32)
+    return fail(MLS_UNSUPPORTED, "in_dtype=%d unsupported", p->in_dtype);
+  if (!(p->tau > 0.0f) || !isfinite(p->tau)) return fail(MLS_INVALID_ARG, "tau must be finite and > 0");
+  if (!isfinite(p->alpha) || p->alpha < 0.0f || p->alpha > 1.0f)
+    return fail(MLS_INVALID_ARG, "alpha must be in [0, 1]");
+  if (p->vocab_chunk < 0) return fail(MLS_INVALID_ARG, "vocab_chunk must be >= 0");
+  if (!p->labels) return fail(MLS_INVALID_ARG, "labels is NULL");
+  if (!aligned(p->labels, 8)) return fail(MLS_INVALID_ARG, "labels not 8-byte aligned");
+  const int64_t gran = p->in_dtype == MLS_BF16 ? 8 : 4;
+  for (int i = 0; i < p->M; ++i) {
+    if (p->d[i] < 1 || p->d[i] > (1 << 20))
+      return fail(MLS_INVALID_ARG, "d[%d]=%lld out of range", i, (long long)p->d[i]);
+    if (p->d[i] % gran)
+      return fail(MLS_UNSUPPORTED, "d[%d]=%lld is not a multiple of %lld", i, (long long)p->d[i],
+                  (long long)gran);
+    if (!p->h[i] || !p->W[i]) return fail(MLS_INVALID_ARG, "h[%d] or W[%d] is NULL", i, i);
+    if (!aligned(p->h[i], 16) || !aligned(p->W[i], 16))
+      return fail(MLS_INVALID_ARG, "h[%d] or W[%d] not 16-byte aligned", i, i);
+  }
+  return MLS_OK;
+}
+
+void make_plan(const mls_problem* p, Plan& pl) {
+  pl.M = p->M;
+  pl.s = p->teacher < 0 ? p->M - 1 : p->teacher;
+  pl.f32 = p->in_dtype == MLS_F32;
+  pl.es = pl.f32 ? 4 : 2;
+  pl.T = p->T;
+  pl.V = p->V;
+  pl.sumd = 0;
+  for (int i = 0; i < p->M; ++i) pl.sumd += p->d[i];
+  pl.T_pad = round_up(p->T, kFusedBN);
+  pl.n_tt = (int)(pl.T_pad / kFusedBN);
+  pl.n_vt_fwd = (int)((p->V + kFusedBM - 1) / kFusedBM);
+  const int64_t vmax = round_up(p->V, 256);
+  int64_t vc;
+  if (p->vocab_chunk > 0) {
+    vc = round_up(p->vocab_chunk, 256);
+  } else {
+    vc = kSlabTargetBytes / (2ll * pl.M * pl.T_pad * pl.es);
+    vc = vc / 256 * 256;
+  }
+  pl.Vc = std::max<int64_t>(256, std::min(vc, vmax));
+  pl.n_chunks = (int)((p->V + pl.Vc - 1) / pl.Vc);
+
+  size_t off = 0;
+  pl.off_partials = off;
+  off = align256(off + (size_t)pl.M * pl.n_vt_fwd * pl.T * sizeof(float4));
+  pl.off_lab = off;
+  off = align256(off + (size_t)pl.M * pl.T * sizeof(float));
+  pl.fwd_bytes = off;
+
+  off = 0;
+  const size_t slab = (size_t)pl.M * pl.T_pad * pl.Vc * pl.es;
+  pl.off_slab = off;
+  off = align256(off + slab);
+  pl.off_slabT = off;
+  off = align256(off + slab);
+  pl.off_hT = off;
+  off = align256(off + (size_t)pl.sumd * pl.T_pad * pl.es);
+  pl.off_WT = off;
+  off = align256(off + (size_t)pl.sumd * pl.Vc * pl.es);
+  pl.bwd_bytes = off;
+  pl.ws_bytes = std::max(pl.fwd_bytes, pl.bwd_bytes);
+
+  pl.header_off = (size_t)(4ll * pl.M * pl.T + pl.T) * sizeof(float);
+  pl.stats_bytes = align256(pl.header_off + 2 * sizeof(int32_t));
+}
+
+void fill_order(const Plan& pl, int32_t* order) {
+  int k = 0;
+  order[k++] = pl.s;
+  for (int i = 0; i < pl.M; ++i)
+    if (i != pl.s) order[k++] = i;
+  for (; k < kMaxModels; ++k) order[k] = 0;
+}
+
+void fill_common(const mls_problem* p, const Plan& pl, FusedArgs& a) {
+  memset(&a, 0, sizeof(a));
+  a.M = pl.M;
+  a.teacher = pl.s;
+  fill_order(pl, a.order);
+  for (int i = 0; i < pl.M; ++i) {
+    a.h[i] = p->h[i];
+    a.W[i] = p->W[i];
+    a.d[i] = p->d[i];
+  }
+  a.T = pl.T;
+  a.V = pl.V;
+  a.labels = p->labels;
+  a.ignore_index = p->ignore_index;
+  a.tau = p->tau;
+  a.inv_tau = 1.0f / p->tau;
+  a.n_tt = pl.n_tt;
+  a.T_pad = pl.T_pad;
+  a.Vc = pl.Vc;
+}
+
+void fill_rows(const mls_problem* p, const Plan& pl, RowArgs& r) {
+  memset(&r, 0, sizeof(r));
+  r.M = pl.M;
+  r.teacher = pl.s;
+  for (int i = 0; i < pl.M; ++i) {
+    r.h[i] = p->h[i];
+    r.W[i] = p->W[i];
+    r.d[i] = p->d[i];
+  }
+  r.T = pl.T;
+  r.V = pl.V;
+  r.labels = p->labels;
+  r.ignore_index = p->ignore_index;
+  r.tau = p->tau;
+  r.n_vt = pl.n_vt_fwd;
+}
+
+void host_coeffs(int M, int s, float alpha, float tau, int mode, const float* w, float* g_ce,
+                 float* g_kl) {
+  for (int i = 0; i < M; ++i) {
+    const float wi = w ? w[i] : 1.0f;
+    if (i == s) {
+      g_ce[i] = wi;
+      g_kl[i] = 0.0f;
+    } else if (mode == MLS_MODE_PAPER) {
+      g_ce[i] = wi * (1.0f - alpha);
+      g_kl[i] = wi * alpha * tau * tau;
+    } else {
+      g_ce[i] = wi;
+      g_kl[i] = wi * alpha * tau * tau;
+    }
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mls_version(void) { return "mls 0.1.0 (gfx950)"; }
+
+const char* mls_last_error(void) { return g_last_error.c_str(); }
+
+const char* mls_status_string(mls_status s) {
+  switch (s) {
+    case MLS_OK: return "ok";
+    case MLS_INVALID_ARG: return "invalid argument";
+    case MLS_UNSUPPORTED: return "unsupported";
+    case MLS_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case MLS_HIP_ERROR: return "HIP error";
+  }
+  return "unknown status";
+}
+
+mls_status mls_query_sizes(const mls_problem* p, size_t* workspace_bytes, size_t* stats_bytes) {
+  g_last_error.clear();
+  mls_status st = validate(p);
+  if (st != MLS_OK) return st;
+  Plan pl;
+  make_plan(p, pl);
+  if (workspace_bytes) *workspace_bytes = pl.ws_bytes;
+  if (stats_bytes) *stats_bytes = pl.stats_bytes;
+  return MLS_OK;
+}
+
+mls_status mls_coeffs(int32_t M, int32_t teacher, float alpha, float tau, int32_t mode,
+                      const float* w, float* g_ce, float* g_kl) {
+  g_last_error.clear();
+  if (M < 1 || M > MLS_MAX_MODELS) return fail(MLS_INVALID_ARG, "M=%d outside [1, %d]", M, MLS_MAX_MODELS);
+  if (teacher < -1 || teacher >= M) return fail(MLS_INVALID_ARG, "teacher=%d outside [-1, M)", teacher);
+  if (!g_ce || !g_kl) return fail(MLS_INVALID_ARG, "output pointer is NULL");
+  if (mode != MLS_MODE_PAPER && mode != MLS_MODE_ADDITIVE)
+    return fail(MLS_INVALID_ARG, "unknown mode %d", mode);
+  if (!(tau > 0.0f) || !isfinite(tau)) return fail(MLS_INVALID_ARG, "tau must be finite and > 0");
+  if (!isfinite(alpha) || alpha < 0.0f || alpha > 1.0f) return fail(MLS_INVALID_ARG, "alpha must be in [0, 1]");
+  host_coeffs(M, teacher < 0 ? M - 1 : teacher, alpha, tau, mode, w, g_ce, g_kl);
+  return MLS_OK;
+}
+
+mls_status mls_distill_fwd(const mls_problem* p, void* stats, float* ce, float* kl, float* entropy,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  mls_status st = validate(p);
+  if (st != MLS_OK) return st;
+  if (!stats || !ce || !kl || !workspace)
+    return fail(MLS_INVALID_ARG, "stats, ce, kl and workspace must be non-NULL");
+  if (!aligned(stats, 16) || !aligned(workspace, 16) || !aligned(ce, 4) || !aligned(kl, 4))
+    return fail(MLS_INVALID_ARG, "misaligned stats / workspace / loss pointer");
+  Plan pl;
+  make_plan(p, pl);
+  if (workspace_bytes < pl.fwd_bytes)
+    return fail(MLS_WORKSPACE_TOO_SMALL, "forward needs %zu workspace bytes, got %zu", pl.fwd_bytes,
+                workspace_bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+
+  FusedArgs a;
+  fill_common(p, pl, a);
+  a.n_vt = pl.n_vt_fwd;
+  a.partials = reinterpret_cast<float4*>(ws + pl.off_partials);
+  hipError_t e;
+  {
+    ProfScope ps("fused_fwd", s);
+    e = launch_fused_fwd(a, pl.f32, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "fused forward launch");
+
+  RowArgs r;
+  fill_rows(p, pl, r);
+  r.partials = a.partials;
+  r.lab = reinterpret_cast<float*>(ws + pl.off_lab);
+  r.stats = static_cast<float*>(stats);
+  r.header = reinterpret_cast<int32_t*>(static_cast<char*>(stats) + pl.header_off);
+  r.ce = ce;
+  r.kl = kl;
+  r.entropy = entropy;
+  {
+    ProfScope ps("label_logits", s);
+    e = launch_label_logits(r, pl.f32, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "label logits launch");
+  {
+    ProfScope ps("row_merge", s);
+    e = launch_finalize_rows(r, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "row merge launch");
+  {
+    ProfScope ps("loss_mean", s);
+    e = launch_reduce_losses(r, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "loss reduction launch");
+  return MLS_OK;
+}
+
+mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float* g_ce,
+                           const float* g_kl, float* const* grad_h, float* const* grad_W,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  mls_status st = validate(p);
+  if (st != MLS_OK) return st;
+  if (!stats || !workspace || !grad_h || !grad_W)
+    return fail(MLS_INVALID_ARG, "stats, workspace, grad_h and grad_W must be non-NULL");
+  if ((g_ce == nullptr) != (g_kl == nullptr))
+    return fail(MLS_INVALID_ARG, "g_ce and g_kl must both be given or both be NULL");
+  if (!aligned(stats, 16) || !aligned(workspace, 16))
+    return fail(MLS_INVALID_ARG, "misaligned stats / workspace");
+  for (int i = 0; i < p->M; ++i) {
+    if ((grad_h[i] && !aligned(grad_h[i], 4)) || (grad_W[i] && !aligned(grad_W[i], 4)))
+      return fail(MLS_INVALID_ARG, "misaligned gradient pointer %d", i);
+  }
+  Plan pl;
+  make_plan(p, pl);
+  if (workspace_bytes < pl.bwd_bytes)
+    return fail(MLS_WORKSPACE_TOO_SMALL, "backward needs %zu workspace bytes, got %zu", pl.bwd_bytes,
+                workspace_bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  const float* sf = static_cast<const float*>(stats);
+
+  FusedArgs a;
+  fill_common(p, pl, a);
+  a.n_vt = (int)(pl.Vc / kFusedBM);
+  a.lse1 = sf;
+  a.lset = sf + (int64_t)pl.M * pl.T;
+  a.n_valid = reinterpret_cast<const int32_t*>(static_cast<const char*>(stats) + pl.header_off);
+  a.g_ce = g_ce;
+  a.g_kl = g_kl;
+  host_coeffs(pl.M, pl.s, p->alpha, p->tau, MLS_MODE_PAPER, nullptr, a.host_gce, a.host_gkl);
+  a.slab = ws + pl.off_slab;
+  a.slabT = ws + pl.off_slabT;
+  char* hT = ws + pl.off_hT;
+  char* WT = ws + pl.off_WT;
+
+  int64_t doff[kMaxModels];
+  int64_t acc = 0;
+  for (int i = 0; i < pl.M; ++i) {
+    doff[i] = acc;
+    acc += p->d[i];
+  }
+  const size_t slab_stride = (size_t)pl.T_pad * pl.Vc * pl.es;
+  hipError_t e;
+
+  // h_i^T [d_i, T_pad] for the grad_W products
+  {
+    TransposeArgs ta;
+    memset(&ta, 0, sizeof(ta));
+    int64_t maxc = 0;
+    for (int i = 0; i < pl.M; ++i) {
+      if (!grad_W[i]) continue;
+      TransposeJob& j = ta.j[ta.njobs++];
+      j.src = p->h[i];
+      j.dst = hT + (size_t)doff[i] * pl.T_pad * pl.es;
+      j.ld_src = p->d[i];
+      j.ld_dst = pl.T_pad;
+      j.r0 = 0;
+      j.src_rows = pl.T;
+      j.out_rows = pl.T_pad;
+      j.cols = p->d[i];
+      maxc = std::max(maxc, p->d[i]);
+    }
+    {
+      ProfScope ps("transpose_h", s);
+      e = launch_transpose(ta, pl.T_pad, maxc, pl.f32, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "transpose launch");
+  }
+
+  for (int c = 0; c < pl.n_chunks; ++c) {
+    const int64_t v0 = (int64_t)c * pl.Vc;
+    const int64_t vrows = std::min(pl.Vc, pl.V - v0);
+
+    // W_i[chunk]^T [d_i, Vc] for the grad_h products
+    TransposeArgs ta;
+    memset(&ta, 0, sizeof(ta));
+    int64_t maxc = 0;
+    for (int i = 0; i < pl.M; ++i) {
+      if (!grad_h[i]) continue;
+      TransposeJob& j = ta.j[ta.njobs++];
+      j.src = p->W[i];
+      j.dst = WT + (size_t)doff[i] * pl.Vc * pl.es;
+      j.ld_src = p->d[i];
+      j.ld_dst = pl.Vc;
+      j.r0 = v0;
+      j.src_rows = pl.V;
+      j.out_rows = pl.Vc;
+      j.cols = p->d[i];
+      maxc = std::max(maxc, p->d[i]);
+    }
+    {
+      ProfScope ps("transpose_W", s);
+      e = launch_transpose(ta, pl.Vc, maxc, pl.f32, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "transpose launch");
+
+    a.v0 = v0;
+    {
+      ProfScope ps("fused_bwd", s);
+      e = launch_fused_bwd(a, pl.f32, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "fused backward launch");
+
+    // grad_W_i[chunk] = G_i^T h_i
+    GemmArgs gw;
+    memset(&gw, 0, sizeof(gw));
+    gw.K = pl.T_pad;
+    int tiles = 0;
+    for (int i = 0; i < pl.M; ++i) {
+      if (!grad_W[i]) continue;
+      GemmGroup& g = gw.g[gw.ngroups++];
+      g.A = static_cast<const char*>(a.slabT) + (size_t)i * slab_stride;
+      g.B = hT + (size_t)doff[i] * pl.T_pad * pl.es;
+      g.C = grad_W[i] + v0 * p->d[i];
+      g.lda = pl.T_pad;
+      g.ldb = pl.T_pad;
+      g.ldc = p->d[i];
+      g.rows = vrows;
+      g.cols = p->d[i];
+      g.tiles_m = (int)((vrows + kGemmBM - 1) / kGemmBM);
+      g.tiles_n = (int)((p->d[i] + kGemmBN - 1) / kGemmBN);
+      g.tile_begin = tiles;
+      g.accumulate = (p->flags & MLS_ACCUMULATE_GRAD_W) ? 1 : 0;
+      tiles += g.tiles_m * g.tiles_n;
+    }
+    {
+      ProfScope ps("gemm_grad_W", s);
+      e = launch_gemm_nt(gw, tiles, pl.f32, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "grad_W launch");
+
+    // grad_h_i (+)= G_i W_i[chunk]
+    GemmArgs gh;
+    memset(&gh, 0, sizeof(gh));
+    gh.K = pl.Vc;
+    tiles = 0;
+    for (int i = 0; i < pl.M; ++i) {
+      if (!grad_h[i]) continue;
+      GemmGroup& g = gh.g[gh.ngroups++];
+      g.A = static_cast<const char*>(a.slab) + (size_t)i * slab_stride;
+      g.B = WT + (size_t)doff[i] * pl.Vc * pl.es;
+      g.C = grad_h[i];
+      g.lda = pl.Vc;
+      g.ldb = pl.Vc;
+      g.ldc = p->d[i];
+      g.rows = pl.T;
+      g.cols = p->d[i];
+      g.tiles_m = (int)((pl.T + kGemmBM - 1) / kGemmBM);
+      g.tiles_n = (int)((p->d[i] + kGemmBN - 1) / kGemmBN);
+      g.tile_begin = tiles;
+      g.accumulate = (c > 0 || (p->flags & MLS_ACCUMULATE_GRAD_H)) ? 1 : 0;
+      tiles += g.tiles_m * g.tiles_n;
+    }
+    {
+      ProfScope ps("gemm_grad_h", s);
+      e = launch_gemm_nt(gh, tiles, pl.f32, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "grad_h launch");
+  }
+  return MLS_OK;
+}
+
+mls_status mls_read_stats_header(const mls_problem* p, const void* stats, void* stream,
+                                 int32_t* n_valid, int32_t* device_flags) {
+  g_last_error.clear();
+  mls_status st = validate(p);
+  if (st != MLS_OK) return st;
+  if (!stats) return fail(MLS_INVALID_ARG, "stats is NULL");
+  Plan pl;
+  make_plan(p, pl);
+  int32_t hdr[2] = {0, 0};
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(hdr, static_cast<const char*>(stats) + pl.header_off, sizeof(hdr),
+                                hipMemcpyDeviceToHost, s);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+  if ((e = hipStreamSynchronize(s)) != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  if (n_valid) *n_valid = hdr[0];
+  if (device_flags) *device_flags = hdr[1];
+  return MLS_OK;
+}
+
+mls_status mls_profile_enable(int32_t enable) {
+  g_last_error.clear();
+  g_prof.on = enable != 0;
+  return MLS_OK;
+}
+
+mls_status mls_profile_report(mls_kernel_time* out, int32_t max_entries, int32_t* n_out) {
+  g_last_error.clear();
+  if (max_entries < 0 || (max_entries > 0 && !out)) return fail(MLS_INVALID_ARG, "bad output array");
+  std::vector<mls_kernel_time> rows;
+  mls_status st = MLS_OK;
+  for (const ProfRec& r : g_prof.recs) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(r.stop);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.start, r.stop);
+    if (e != hipSuccess && st == MLS_OK) st = hip_fail(e, "kernel timing");
+    size_t k = 0;
+    for (; k < rows.size(); ++k)
+      if (strncmp(rows[k].name, r.name, sizeof(rows[k].name)) == 0) break;
+    if (k == rows.size()) {
+      mls_kernel_time t;
+      memset(&t, 0, sizeof(t));
+      strncpy(t.name, r.name, sizeof(t.name) - 1);
+      rows.push_back(t);
+    }
+    rows[k].launches += 1;
+    rows[k].total_ms += ms;
+    g_prof.pool.push_back(r.start);
+    g_prof.pool.push_back(r.stop);
+  }
+  g_prof.recs.clear();
+  const int32_t n = (int32_t)std::min<size_t>(rows.size(), (size_t)max_entries);
+  for (int32_t k = 0; k < n; ++k) out[k] = rows[k];
+  if (n_out) *n_out = (int32_t)rows.size();
+  return st;
+}
+
+}  // extern "C"

@@ -1,0 +1,288 @@
+// Fused LM-head logits kernels: one block owns a 128 (vocabulary) x 128 (token)
+// tile and computes it for every sub-model, teacher first.
+//
+// Forward (per tile, per sub-model i, per token t): the online log-sum-exp
+// statistics of paper section 2 ("Modeling": logits of every head;
+// "Integrated Distillation": eq. (2) needs the teacher's softmax next to every
+// student's). The teacher's tile is computed first and its exponentials
+// e_v = exp((l_s,v - max) / tau) stay in registers, laid out exactly like the
+// accumulators of the students' tiles, so each student adds its cross term
+// sum_v e_v l_i,v with no extra memory traffic. Only per-tile partial rows
+// (max, sum exp, sum exp / tau, cross term) leave the block.
+//
+// Backward (per vocabulary chunk): logits are recomputed tile by tile, the
+// teacher's q = softmax(l_s / tau) is formed once per tile and reused by every
+// student, and the logit gradient
+//   G_i = ( g_ce,i (softmax(l_i) - onehot(y)) + g_kl,i / tau (softmax(l_i / tau) - q) ) / N
+// (eq. (2) with stop_grad on q, eq. (3) through the coefficients) is written
+// to the chunk slab in two layouts for the two backward GEMMs.
+#include <math.h>
+
+#include "mls_device.h"
+#include "mls_launch.h"
+
+namespace mls {
+
+namespace {
+
+constexpr int BM = kFusedBM;
+constexpr int BN = kFusedBN;
+constexpr int WGM = 2;
+constexpr int WGN = 2;
+
+template <typename E, bool TAU1>
+__global__ __launch_bounds__(kThreads, 2) void fused_fwd_kernel(FusedArgs a) {
+  using Mma = TileMma<E, BM, BN, WGM, WGN>;
+  constexpr int FM = Mma::FM;
+  constexpr int FN = Mma::FN;
+  __shared__ __attribute__((aligned(16))) char smem[Mma::kSmemBytes];
+  __shared__ float red[WGM][BN][4];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave % WGM;
+  const int wn = wave / WGM;
+  const int hi = lane >> 5;
+  const int tt = blockIdx.x % a.n_tt;
+  const int vt = blockIdx.x / a.n_tt;
+  const int64_t vbase = (int64_t)vt * BM;
+  const int64_t tbase = (int64_t)tt * BN;
+  const bool full = vbase + BM <= a.V;
+  const float ct = kLog2e * a.inv_tau;
+
+  float e_t[FM][FN][16];  // teacher weights exp((l_s - max_s) / tau); 0 outside V
+  Mma mma;
+
+  for (int oi = 0; oi < a.M; ++oi) {
+    const int i = a.order[oi];
+    const int64_t kb = a.d[i] * E::kBytes;
+    mma.run(static_cast<const char*>(a.W[i]), kb, vbase, a.V, static_cast<const char*>(a.h[i]),
+            kb, tbase, a.T, kb, smem, tid);
+
+    // 1. block max of each token column over the tile's valid vocabulary rows
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      float m = -INFINITY;
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const bool ok = full || vbase + Mma::row_of(wm, fm, r, lane) < a.V;
+          if (ok) m = fmaxf(m, mma.acc[fm][fn][r]);
+        }
+      m = fmaxf(m, shfl_xor32(m));
+      if (hi == 0) red[wm][Mma::col_of(wn, fn, lane)][0] = m;
+    }
+    __syncthreads();
+    float mb[FN];
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      const int c = Mma::col_of(wn, fn, lane);
+      float m = red[0][c][0];
+#pragma unroll
+      for (int w = 1; w < WGM; ++w) m = fmaxf(m, red[w][c][0]);
+      mb[fn] = m;
+    }
+
+    // 2. sums relative to the block max
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      float s1 = 0.f, st = 0.f, xr = 0.f;
+      if (oi == 0) {
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const bool ok = full || vbase + Mma::row_of(wm, fm, r, lane) < a.V;
+            const float l = mma.acc[fm][fn][r];
+            const float x = l - mb[fn];
+            const float e = ok ? fast_exp2(x * ct) : 0.f;
+            e_t[fm][fn][r] = e;
+            st += e;
+            xr = fmaf(e, l, xr);
+            if (!TAU1) s1 += ok ? fast_exp2(x * kLog2e) : 0.f;
+          }
+        if (TAU1) s1 = st;
+      } else {
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const bool ok = full || vbase + Mma::row_of(wm, fm, r, lane) < a.V;
+            const float l = mma.acc[fm][fn][r];
+            const float x = l - mb[fn];
+            s1 += ok ? fast_exp2(x * kLog2e) : 0.f;
+            if (!TAU1) st += ok ? fast_exp2(x * ct) : 0.f;
+            xr = fmaf(e_t[fm][fn][r], l, xr);
+          }
+        if (TAU1) st = s1;
+      }
+      s1 += shfl_xor32(s1);
+      st += shfl_xor32(st);
+      xr += shfl_xor32(xr);
+      if (hi == 0) {
+        const int c = Mma::col_of(wn, fn, lane);
+        red[wm][c][1] = s1;
+        red[wm][c][2] = st;
+        red[wm][c][3] = xr;
+      }
+    }
+    __syncthreads();
+
+    // 3. one partial row per token
+    if (tid < BN) {
+      const int64_t t = tbase + tid;
+      if (t < a.T) {
+        float m = red[0][tid][0], s1 = red[0][tid][1], st = red[0][tid][2], xr = red[0][tid][3];
+#pragma unroll
+        for (int w = 1; w < WGM; ++w) {
+          m = fmaxf(m, red[w][tid][0]);
+          s1 += red[w][tid][1];
+          st += red[w][tid][2];
+          xr += red[w][tid][3];
+        }
+        a.partials[((int64_t)i * a.n_vt + vt) * a.T + t] = make_float4(m, s1, st, xr);
+      }
+    }
+    // `red` is rewritten only after the next tile product, which synchronises.
+  }
+}
+
+template <typename E>
+__device__ __forceinline__ void store4(typename E::storage* p, float a0, float a1, float a2,
+                                       float a3);
+template <>
+__device__ __forceinline__ void store4<Bf16>(uint16_t* p, float a0, float a1, float a2,
+                                             float a3) {
+  uint2 v;
+  v.x = (uint32_t)to_storage<Bf16>(a0) | ((uint32_t)to_storage<Bf16>(a1) << 16);
+  v.y = (uint32_t)to_storage<Bf16>(a2) | ((uint32_t)to_storage<Bf16>(a3) << 16);
+  *reinterpret_cast<uint2*>(p) = v;
+}
+template <>
+__device__ __forceinline__ void store4<F32>(float* p, float a0, float a1, float a2, float a3) {
+  *reinterpret_cast<float4*>(p) = make_float4(a0, a1, a2, a3);
+}
+
+template <typename E, bool TAU1>
+__global__ __launch_bounds__(kThreads, 1) void fused_bwd_kernel(FusedArgs a) {
+  using Mma = TileMma<E, BM, BN, WGM, WGN>;
+  using S = typename E::storage;
+  constexpr int FM = Mma::FM;
+  constexpr int FN = Mma::FN;
+  __shared__ __attribute__((aligned(16))) char smem[Mma::kSmemBytes];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave % WGM;
+  const int wn = wave / WGM;
+  const int tt = blockIdx.x % a.n_tt;
+  const int vt = blockIdx.x / a.n_tt;
+  const int64_t vloc = (int64_t)vt * BM;  // row offset inside the chunk
+  const int64_t vbase = a.v0 + vloc;      // absolute vocabulary row
+  const int64_t tbase = (int64_t)tt * BN;
+  const bool full = vbase + BM <= a.V;
+  const int nv = *a.n_valid;
+  const float invN = nv > 0 ? 1.0f / (float)nv : 0.0f;
+
+  int64_t tok[FN];
+  int ylab[FN];  // label row relative to the tile, or -1
+  bool rv[FN];
+#pragma unroll
+  for (int fn = 0; fn < FN; ++fn) {
+    const int64_t t = tbase + Mma::col_of(wn, fn, lane);
+    tok[fn] = t;
+    const int64_t y = t < a.T ? a.labels[t] : a.ignore_index;
+    rv[fn] = t < a.T && y != a.ignore_index && y >= 0 && y < a.V;
+    const int64_t rel = y - vbase;
+    ylab[fn] = (rv[fn] && rel >= 0 && rel < BM) ? (int)rel : -1;
+  }
+
+  float q_t[FM][FN][16];  // teacher softmax at tau; 0 outside V and on invalid rows
+  Mma mma;
+
+  for (int oi = 0; oi < a.M; ++oi) {
+    const int i = a.order[oi];
+    const int64_t kb = a.d[i] * E::kBytes;
+    mma.run(static_cast<const char*>(a.W[i]), kb, vbase, a.V, static_cast<const char*>(a.h[i]),
+            kb, tbase, a.T, kb, smem, tid);
+    const float gce = a.g_ce ? a.g_ce[i] : a.host_gce[i];
+    const float gkl = a.g_kl ? a.g_kl[i] : a.host_gkl[i];
+    S* slab = static_cast<S*>(a.slab) + (int64_t)i * a.T_pad * a.Vc;
+    S* slabT = static_cast<S*>(a.slabT) + (int64_t)i * a.T_pad * a.Vc;
+
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      const int64_t t = tok[fn];
+      // invalid rows: +inf log-normalisers make every probability 0
+      const float l1 = rv[fn] ? a.lse1[(int64_t)i * a.T + t] : INFINITY;
+      const float lt = rv[fn] ? a.lset[(int64_t)i * a.T + t] : INFINITY;
+      const float cg = rv[fn] ? gce * invN : 0.f;
+      const float ck = (rv[fn] && oi != 0) ? gkl * invN * a.inv_tau : 0.f;
+      const float l1s = l1 * kLog2e;
+      const float lts = lt * kLog2e;
+      const float ct = kLog2e * a.inv_tau;
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+          float g[4];
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) {
+            const int r = rg * 4 + rr;
+            const int row = Mma::row_of(wm, fm, r, lane);
+            const bool ok = full || vbase + row < a.V;
+            const float l = mma.acc[fm][fn][r];
+            const float oh = row == ylab[fn] ? 1.f : 0.f;
+            if (oi == 0) {
+              const float q = ok ? fast_exp2(fmaf(l, ct, -lts)) : 0.f;
+              q_t[fm][fn][r] = q;
+              const float p1 = TAU1 ? q : (ok ? fast_exp2(fmaf(l, kLog2e, -l1s)) : 0.f);
+              g[rr] = cg * (p1 - oh);
+            } else {
+              const float p1 = ok ? fast_exp2(fmaf(l, kLog2e, -l1s)) : 0.f;
+              const float pt = TAU1 ? p1 : (ok ? fast_exp2(fmaf(l, ct, -lts)) : 0.f);
+              g[rr] = fmaf(cg, p1 - oh, ck * (pt - q_t[fm][fn][r]));
+            }
+          }
+          const int row0 = Mma::row_of(wm, fm, rg * 4, lane);
+          store4<E>(slab + t * a.Vc + vloc + row0, g[0], g[1], g[2], g[3]);
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr)
+            slabT[(vloc + row0 + rr) * a.T_pad + t] = to_storage<E>(g[rr]);
+        }
+    }
+  }
+}
+
+template <typename E, bool TAU1>
+hipError_t launch_fwd_t(const FusedArgs& a, hipStream_t stream) {
+  dim3 grid((unsigned)a.n_tt * (unsigned)a.n_vt);
+  hipLaunchKernelGGL((fused_fwd_kernel<E, TAU1>), grid, dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+template <typename E, bool TAU1>
+hipError_t launch_bwd_t(const FusedArgs& a, hipStream_t stream) {
+  dim3 grid((unsigned)a.n_tt * (unsigned)a.n_vt);
+  hipLaunchKernelGGL((fused_bwd_kernel<E, TAU1>), grid, dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_fused_fwd(const FusedArgs& a, bool f32, hipStream_t stream) {
+  const bool tau1 = a.tau == 1.0f;
+  if (f32) return tau1 ? launch_fwd_t<F32, true>(a, stream) : launch_fwd_t<F32, false>(a, stream);
+  return tau1 ? launch_fwd_t<Bf16, true>(a, stream) : launch_fwd_t<Bf16, false>(a, stream);
+}
+
+hipError_t launch_fused_bwd(const FusedArgs& a, bool f32, hipStream_t stream) {
+  const bool tau1 = a.tau == 1.0f;
+  if (f32) return tau1 ? launch_bwd_t<F32, true>(a, stream) : launch_bwd_t<F32, false>(a, stream);
+  return tau1 ? launch_bwd_t<Bf16, true>(a, stream) : launch_bwd_t<Bf16, false>(a, stream);
+}
+
+}  // namespace mls

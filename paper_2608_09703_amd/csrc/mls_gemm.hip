@@ -1,0 +1,108 @@
+// The two backward products of the LM head (the head is linear, paper
+// section 2, "Modeling"), per vocabulary chunk and for every sub-model in one
+// grouped launch:
+//   grad_W_i[chunk] = G_i^T h_i       A = G_i^T slab [Vc, T_pad], B = h_i^T [d_i, T_pad]
+//   grad_h_i       += G_i W_i[chunk]  A = G_i slab   [T_pad, Vc], B = W_i[chunk]^T [d_i, Vc]
+// Both are NT tile products on the shared MFMA main loop; the transposed
+// operands h_i^T and W_i[chunk]^T are produced by the transpose kernel below.
+#include "mls_device.h"
+#include "mls_launch.h"
+
+namespace mls {
+
+namespace {
+
+template <typename E>
+__global__ __launch_bounds__(kThreads, 2) void gemm_nt_kernel(GemmArgs a) {
+  using Mma = TileMma<E, kGemmBM, kGemmBN, 2, 2>;
+  constexpr int FM = Mma::FM;
+  constexpr int FN = Mma::FN;
+  __shared__ __attribute__((aligned(16))) char smem[Mma::kSmemBytes];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave % 2;
+  const int wn = wave / 2;
+  const int b = blockIdx.x;
+  int gi = 0;
+  for (int k = 1; k < a.ngroups; ++k)
+    if (b >= a.g[k].tile_begin) gi = k;
+  const GemmGroup& g = a.g[gi];
+  const int local = b - g.tile_begin;
+  const int tm = local % g.tiles_m;
+  const int tn = local / g.tiles_m;
+  const int64_t m0 = (int64_t)tm * kGemmBM;
+  const int64_t n0 = (int64_t)tn * kGemmBN;
+
+  Mma mma;
+  mma.run(static_cast<const char*>(g.A), g.lda * E::kBytes, m0, g.rows,
+          static_cast<const char*>(g.B), g.ldb * E::kBytes, n0, g.cols, a.K * E::kBytes, smem,
+          tid);
+
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      const int64_t n = n0 + Mma::col_of(wn, fn, lane);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t m = m0 + Mma::row_of(wm, fm, r, lane);
+        if (m < g.rows && n < g.cols) {
+          float* c = g.C + m * g.ldc + n;
+          *c = g.accumulate ? *c + mma.acc[fm][fn][r] : mma.acc[fm][fn][r];
+        }
+      }
+    }
+}
+
+template <typename S>
+__global__ __launch_bounds__(kThreads) void transpose_kernel(TransposeArgs a) {
+  const TransposeJob& j = a.j[blockIdx.z];
+  const int64_t rb = (int64_t)blockIdx.x * 64;
+  const int64_t cb = (int64_t)blockIdx.y * 64;
+  if (rb >= j.out_rows || cb >= j.cols) return;
+  __shared__ S tile[64][65];
+  const int tx = threadIdx.x & 63;
+  const int ty = threadIdx.x >> 6;
+  const S* src = static_cast<const S*>(j.src);
+  S* dst = static_cast<S*>(j.dst);
+  for (int rr = ty; rr < 64; rr += 4) {
+    const int64_t r = rb + rr;
+    const int64_t c = cb + tx;
+    S v = S(0);
+    if (r < j.out_rows && c < j.cols && j.r0 + r < j.src_rows) v = src[(j.r0 + r) * j.ld_src + c];
+    tile[rr][tx] = v;
+  }
+  __syncthreads();
+  for (int cc = ty; cc < 64; cc += 4) {
+    const int64_t c = cb + cc;
+    const int64_t r = rb + tx;
+    if (c < j.cols && r < j.out_rows) dst[c * j.ld_dst + r] = tile[tx][cc];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_gemm_nt(const GemmArgs& a, int total_tiles, bool f32, hipStream_t stream) {
+  if (total_tiles <= 0) return hipSuccess;
+  if (f32)
+    hipLaunchKernelGGL(gemm_nt_kernel<F32>, dim3(total_tiles), dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(gemm_nt_kernel<Bf16>, dim3(total_tiles), dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose(const TransposeArgs& a, int64_t max_out_rows, int64_t max_cols,
+                            bool f32, hipStream_t stream) {
+  if (a.njobs <= 0) return hipSuccess;
+  dim3 grid((unsigned)((max_out_rows + 63) / 64), (unsigned)((max_cols + 63) / 64),
+            (unsigned)a.njobs);
+  if (f32)
+    hipLaunchKernelGGL(transpose_kernel<float>, grid, dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(transpose_kernel<uint16_t>, grid, dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace mls

@@ -1,0 +1,131 @@
+// Launch descriptors shared by the host planner (mls_api.cpp) and the kernel
+// translation units. Plain structs passed by value as kernel arguments.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "mls.h"
+
+namespace mls {
+
+constexpr int kMaxModels = 8;
+
+// Tile of the fused logits kernels: BM vocabulary rows x BN token columns.
+constexpr int kFusedBM = 128;
+constexpr int kFusedBN = 128;
+// Tile of the backward GEMMs.
+constexpr int kGemmBM = 128;
+constexpr int kGemmBN = 128;
+
+// Per-row partial statistics of one (sub-model, vocabulary tile, token):
+//   x = max logit over the tile's vocabulary rows (own max)
+//   y = sum exp(l - x)            (tau = 1)
+//   z = sum exp((l - x) / tau)
+//   w = sum e_v * l_v with e_v = exp((l_s,v - x_s) / tau) the teacher's
+//       weights relative to the teacher's max x_s of the same tile
+// (w of the teacher itself uses its own logits).
+struct FusedArgs {
+  int32_t M;
+  int32_t teacher;
+  int32_t order[kMaxModels];  // processing order; order[0] is the teacher
+  const void* h[kMaxModels];
+  const void* W[kMaxModels];
+  int64_t d[kMaxModels];
+  int64_t T;
+  int64_t V;
+  const int64_t* labels;
+  int64_t ignore_index;
+  float tau;
+  float inv_tau;
+  int32_t n_tt;  // token tiles
+  int32_t n_vt;  // vocabulary tiles in this launch
+  // forward
+  float4* partials;  // [M][n_vt][T]
+  // backward
+  const float* lse1;  // [M][T]
+  const float* lset;  // [M][T]
+  const int32_t* n_valid;
+  const float* g_ce;  // device [M] or null
+  const float* g_kl;
+  float host_gce[kMaxModels];
+  float host_gkl[kMaxModels];
+  void* slab;   // [M][T_pad][Vc]  dJ/dlogits, token-major
+  void* slabT;  // [M][Vc][T_pad]  dJ/dlogits, vocabulary-major
+  int64_t T_pad;
+  int64_t Vc;
+  int64_t v0;  // first vocabulary row of the chunk
+};
+
+// One output matrix of a grouped NT GEMM: C[m][n] (+)= sum_k A[m][k] B[n][k].
+struct GemmGroup {
+  const void* A;
+  const void* B;
+  float* C;
+  int64_t lda;  // elements
+  int64_t ldb;
+  int64_t ldc;
+  int64_t rows;  // m extent
+  int64_t cols;  // n extent
+  int32_t tiles_m;
+  int32_t tiles_n;
+  int32_t tile_begin;
+  int32_t accumulate;
+};
+
+struct GemmArgs {
+  int32_t ngroups;
+  int64_t K;  // contraction length in elements (a multiple of the LDS row)
+  GemmGroup g[kMaxModels];
+};
+
+// dst[c][r] = src[(r0 + r) * ld_src + c] for r0 + r < src_rows, else 0;
+// r < out_rows, c < cols; dst row stride ld_dst.
+struct TransposeJob {
+  const void* src;
+  void* dst;
+  int64_t ld_src;
+  int64_t ld_dst;
+  int64_t r0;
+  int64_t src_rows;
+  int64_t out_rows;
+  int64_t cols;
+};
+
+struct TransposeArgs {
+  int32_t njobs;
+  TransposeJob j[kMaxModels];
+};
+
+struct RowArgs {
+  int32_t M;
+  int32_t teacher;
+  const void* h[kMaxModels];
+  const void* W[kMaxModels];
+  int64_t d[kMaxModels];
+  int64_t T;
+  int64_t V;
+  const int64_t* labels;
+  int64_t ignore_index;
+  float tau;
+  int32_t n_vt;
+  const float4* partials;  // [M][n_vt][T]
+  float* lab;              // [M][T] label logits
+  float* stats;            // lse1, lset, ce_row, kl_row, h_row
+  int32_t* header;         // n_valid, flags
+  float* ce;
+  float* kl;
+  float* entropy;
+};
+
+// Launchers (each enqueues on `stream` and returns the launch status).
+hipError_t launch_fused_fwd(const FusedArgs& a, bool f32, hipStream_t stream);
+hipError_t launch_fused_bwd(const FusedArgs& a, bool f32, hipStream_t stream);
+hipError_t launch_gemm_nt(const GemmArgs& a, int total_tiles, bool f32, hipStream_t stream);
+hipError_t launch_transpose(const TransposeArgs& a, int64_t max_out_rows, int64_t max_cols,
+                            bool f32, hipStream_t stream);
+hipError_t launch_label_logits(const RowArgs& a, bool f32, hipStream_t stream);
+hipError_t launch_finalize_rows(const RowArgs& a, hipStream_t stream);
+hipError_t launch_reduce_losses(const RowArgs& a, hipStream_t stream);
+
+}  // namespace mls

@@ -1,0 +1,160 @@
+"""PyTorch front end of the fused multi-sub-model LM head + CE + KL.
+
+``distill(h_list, W_list, labels, ...)`` returns the per-sub-model
+cross-entropies ``ce[M]``, the distillation values ``kl[M]`` (KL from the
+teacher's softmax at temperature tau) and the mean teacher entropy, with
+autograd support: the backward pass feeds the upstream gradients of ``ce``
+and ``kl`` to the library as the coefficients of the objective, so any
+objective linear in them (eq. (3) of the paper with its sum over
+sub-models, or per-sub-model weights) differentiates correctly with no host
+synchronisation.
+
+``forward`` / ``backward`` are the same two library calls without autograd,
+on caller-visible buffers (used by the tests and the benchmark).
+"""
+
+from __future__ import annotations
+
+from typing import List, Optional, Sequence
+
+import torch
+
+from . import binding as B
+
+
+def _dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.bfloat16:
+        return B.MLS_BF16
+    if dt == torch.float32:
+        return B.MLS_F32
+    raise TypeError(f"unsupported dtype {dt}; use bfloat16 or float32")
+
+
+def make_problem(h: Sequence[torch.Tensor], W: Sequence[torch.Tensor], labels: torch.Tensor, *,
+                 alpha: float = 0.0, tau: float = 1.0, teacher: int = -1,
+                 ignore_index: int = -100, flags: int = 0, vocab_chunk: int = 0) -> B.Problem:
+    M = len(h)
+    if M < 1 or len(W) != M:
+        raise ValueError("need one head per sub-model")
+    dev = h[0].device
+    if dev.type != "cuda":
+        raise RuntimeError("the fused loss runs on the GPU only; got tensors on " + str(dev))
+    dt = h[0].dtype
+    T = h[0].shape[0]
+    V = W[0].shape[0]
+    for i in range(M):
+        for x in (h[i], W[i]):
+            if x.device != dev or x.dtype != dt or x.dim() != 2 or not x.is_contiguous():
+                raise ValueError("h_i / W_i must be contiguous 2-D tensors of one dtype on one device")
+        if h[i].shape[0] != T or W[i].shape[0] != V or h[i].shape[1] != W[i].shape[1]:
+            raise ValueError(f"shape mismatch in sub-model {i}")
+    if labels.device != dev or labels.dtype != torch.int64 or labels.shape != (T,) \
+            or not labels.is_contiguous():
+        raise ValueError("labels must be a contiguous int64 [T] tensor on the same device")
+    return B.make_problem(M, T, V, [x.shape[1] for x in h], [x.data_ptr() for x in h],
+                          [x.data_ptr() for x in W], labels.data_ptr(), dtype=_dtype_code(dt),
+                          teacher=teacher, ignore_index=ignore_index, alpha=alpha, tau=tau,
+                          flags=flags, vocab_chunk=vocab_chunk)
+
+
+def _stream(dev) -> int:
+    return torch.cuda.current_stream(dev).cuda_stream
+
+
+class Buffers:
+    """Caller-owned device buffers of one problem shape (workspace + statistics)."""
+
+    def __init__(self, p: B.Problem, device):
+        self.ws_bytes, self.stats_bytes = B.query_sizes(p)
+        self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=device)
+        self.stats = torch.empty(self.stats_bytes, dtype=torch.uint8, device=device)
+        M = p.M
+        self.ce = torch.empty(M, dtype=torch.float32, device=device)
+        self.kl = torch.empty(M, dtype=torch.float32, device=device)
+        self.entropy = torch.empty(1, dtype=torch.float32, device=device)
+
+    def stats_view(self, M: int, T: int):
+        """(lse1, lset, ce_row, kl_row, h_row) views into the statistics buffer."""
+        f = self.stats[: (4 * M * T + T) * 4].view(torch.float32)
+        return (f[: M * T].view(M, T), f[M * T: 2 * M * T].view(M, T),
+                f[2 * M * T: 3 * M * T].view(M, T), f[3 * M * T: 4 * M * T].view(M, T),
+                f[4 * M * T:])
+
+
+def forward(p: B.Problem, buf: Buffers, device) -> None:
+    B.distill_fwd(p, buf.stats.data_ptr(), buf.ce.data_ptr(), buf.kl.data_ptr(),
+                  buf.entropy.data_ptr(), buf.workspace.data_ptr(), buf.workspace.numel(),
+                  _stream(device))
+
+
+def backward(p: B.Problem, buf: Buffers, device, g_ce: Optional[torch.Tensor],
+             g_kl: Optional[torch.Tensor], grad_h: Sequence[Optional[torch.Tensor]],
+             grad_W: Sequence[Optional[torch.Tensor]]) -> None:
+    for g in list(grad_h) + list(grad_W):
+        if g is not None and (g.dtype != torch.float32 or not g.is_contiguous()):
+            raise ValueError("gradients are contiguous float32 tensors")
+    gc = g_ce.data_ptr() if g_ce is not None else None
+    gk = g_kl.data_ptr() if g_kl is not None else None
+    B.distill_bwd(p, buf.stats.data_ptr(), gc, gk,
+                  [g.data_ptr() if g is not None else None for g in grad_h],
+                  [g.data_ptr() if g is not None else None for g in grad_W],
+                  buf.workspace.data_ptr(), buf.workspace.numel(), _stream(device))
+
+
+class _Distill(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, labels, opts, *hw):
+        M = len(hw) // 2
+        h, W = list(hw[:M]), list(hw[M:])
+        p = make_problem(h, W, labels, **opts)
+        dev = h[0].device
+        buf = Buffers(p, dev)
+        forward(p, buf, dev)
+        ctx.p = p
+        ctx.buf = buf
+        ctx.M = M
+        ctx.save_for_backward(labels, *hw)
+        ctx.mark_non_differentiable(buf.entropy)
+        return buf.ce.clone(), buf.kl.clone(), buf.entropy.clone()
+
+    @staticmethod
+    def backward(ctx, g_ce, g_kl, g_ent):
+        saved = ctx.saved_tensors
+        hw = saved[1:]
+        M = ctx.M
+        dev = hw[0].device
+        if g_ce is None:
+            g_ce = torch.zeros(M, dtype=torch.float32, device=dev)
+        if g_kl is None:
+            g_kl = torch.zeros(M, dtype=torch.float32, device=dev)
+        g_ce = g_ce.to(torch.float32).contiguous()
+        g_kl = g_kl.to(torch.float32).contiguous()
+        need = ctx.needs_input_grad[2:]
+        gh: List[Optional[torch.Tensor]] = []
+        gW: List[Optional[torch.Tensor]] = []
+        for i in range(M):
+            gh.append(torch.empty(hw[i].shape, dtype=torch.float32, device=dev) if need[i] else None)
+            gW.append(torch.empty(hw[M + i].shape, dtype=torch.float32, device=dev)
+                      if need[M + i] else None)
+        backward(ctx.p, ctx.buf, dev, g_ce, g_kl, gh, gW)
+        out = [None, None]
+        for i in range(M):
+            out.append(gh[i].to(hw[i].dtype) if gh[i] is not None else None)
+        for i in range(M):
+            out.append(gW[i].to(hw[M + i].dtype) if gW[i] is not None else None)
+        return tuple(out)
+
+
+def distill(h_list: Sequence[torch.Tensor], W_list: Sequence[torch.Tensor], labels: torch.Tensor,
+            *, tau: float = 1.0, teacher: int = -1, ignore_index: int = -100,
+            vocab_chunk: int = 0):
+    """Per-sub-model ``(ce[M], kl[M], entropy[1])`` with autograd through the HIP kernels."""
+    opts = dict(tau=tau, teacher=teacher, ignore_index=ignore_index, vocab_chunk=vocab_chunk)
+    return _Distill.apply(labels, opts, *h_list, *W_list)
+
+
+def coefficients(M: int, *, alpha: float, tau: float = 1.0, teacher: int = -1,
+                 mode: str = "paper", weights: Optional[Sequence[float]] = None):
+    """``(g_ce, g_kl)`` lists of eq. (3) (``mode="paper"``) or the additive form."""
+    m = B.MLS_MODE_PAPER if mode == "paper" else B.MLS_MODE_ADDITIVE
+    return B.coeffs(M, teacher, alpha, tau, m, weights)

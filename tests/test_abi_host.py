@@ -1,0 +1,164 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+The library loads without a GPU; every argument error is detected on the
+host before any device call, so these calls never touch the device.
+"""
+
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_09703_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "mls.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(mls_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = B.lib()
+    names = _declared_functions()
+    assert set(names) == set(B.EXPORTED)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_version_and_status_strings():
+    assert "gfx950" in B.version()
+    L = B.lib()
+    assert L.mls_status_string(B.MLS_OK) == b"ok"
+    assert L.mls_status_string(B.MLS_WORKSPACE_TOO_SMALL) == b"workspace too small"
+
+
+def test_problem_struct_layout_matches_header(tmp_path):
+    """The ctypes mirror of mls_problem has the C compiler's layout."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    fields = [f[0] for f in B.Problem._fields_]
+    prog = tmp_path / "layout.c"
+    body = "".join(f'printf("%zu\\n", offsetof(mls_problem, {f}));' for f in fields)
+    prog.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "mls.h"\n'
+                    'int main(void){printf("%zu\\n", sizeof(mls_problem));' + body + 'return 0;}')
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-I", os.path.join(ROOT, "include"), str(prog), "-o", str(exe)], check=True)
+    out = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True,
+                                          check=True).stdout.split()]
+    assert out[0] == ctypes.sizeof(B.Problem)
+    for f, off in zip(fields, out[1:]):
+        assert getattr(B.Problem, f).offset == off, f
+
+
+@pytest.mark.parametrize("mode", [B.MLS_MODE_PAPER, B.MLS_MODE_ADDITIVE])
+@pytest.mark.parametrize("teacher", [-1, 0, 2])
+def test_coeffs_match_oracle(mode, teacher):
+    w = [0.5, 1.5, 2.0]
+    g_ce, g_kl = B.coeffs(3, teacher, 0.3, 2.0, mode, w)
+    o_ce, o_kl = oracle.coeffs(3, teacher, 0.3, 2.0, "paper" if mode == 0 else "additive", w)
+    np.testing.assert_allclose(g_ce, o_ce, rtol=1e-6)
+    np.testing.assert_allclose(g_kl, o_kl, rtol=1e-6)
+
+
+def _fake_problem(**kw):
+    M = kw.pop("M", 3)
+    dims = kw.pop("dims", [1024, 2048, 3072][:M] + [64] * max(0, M - 3))
+    base = 1 << 32  # fake, 256-aligned addresses; never dereferenced by these tests
+    return B.make_problem(M, kw.pop("T", 4096), kw.pop("V", 50304), dims,
+                          [base + 0x100000 * i for i in range(M)],
+                          [base + 0x10000000 + 0x100000 * i for i in range(M)], base + 0x20000000,
+                          **kw)
+
+
+def test_query_sizes_reports_workspace_and_stats():
+    p = _fake_problem()
+    ws, st = B.query_sizes(p)
+    M, T = 3, 4096
+    assert st >= (4 * M * T + T) * 4 + 8
+    assert ws >= M * ((50304 + 127) // 128) * T * 16  # forward partial rows
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("M", 0, B.MLS_INVALID_ARG),
+    ("M", 9, B.MLS_INVALID_ARG),
+    ("teacher", 3, B.MLS_INVALID_ARG),
+    ("T", 0, B.MLS_INVALID_ARG),
+    ("V", 1, B.MLS_INVALID_ARG),
+    ("tau", 0.0, B.MLS_INVALID_ARG),
+    ("tau", -1.0, B.MLS_INVALID_ARG),
+    ("tau", math.inf, B.MLS_INVALID_ARG),
+    ("alpha", math.nan, B.MLS_INVALID_ARG),
+    ("alpha", 1.5, B.MLS_INVALID_ARG),
+    ("in_dtype", 7, B.MLS_UNSUPPORTED),
+    ("vocab_chunk", -5, B.MLS_INVALID_ARG),
+    ("labels", None, B.MLS_INVALID_ARG),
+])
+def test_invalid_arguments_rejected_on_host(field, value, status):
+    p = _fake_problem()
+    setattr(p, field, value)
+    ws = ctypes.c_size_t(0)
+    st = ctypes.c_size_t(0)
+    got = B.lib().mls_query_sizes(ctypes.byref(p), ctypes.byref(ws), ctypes.byref(st))
+    assert got == status
+    assert B.lib().mls_last_error() != b""
+
+
+def test_width_granularity_and_alignment():
+    p = _fake_problem(dims=[1024, 2048, 3070])
+    with pytest.raises(B.MlsError) as e:
+        B.query_sizes(p)
+    assert e.value.status == B.MLS_UNSUPPORTED
+    p = _fake_problem(dtype=B.MLS_F32, dims=[1024, 2048, 3068])
+    B.query_sizes(p)  # fp32 needs only multiples of 4
+    p = _fake_problem()
+    p.h[1] = p.h[1] + 8
+    with pytest.raises(B.MlsError) as e:
+        B.query_sizes(p)
+    assert e.value.status == B.MLS_INVALID_ARG
+    p = _fake_problem()
+    p.W[0] = None
+    with pytest.raises(B.MlsError):
+        B.query_sizes(p)
+
+
+def test_forward_rejects_small_workspace_before_device_work():
+    p = _fake_problem()
+    ws, st = B.query_sizes(p)
+    fake = 1 << 40
+    with pytest.raises(B.MlsError) as e:
+        B.distill_fwd(p, fake, fake + 4096, fake + 8192, None, fake + (1 << 20), 1024, None)
+    assert e.value.status == B.MLS_WORKSPACE_TOO_SMALL
+    with pytest.raises(B.MlsError) as e:
+        B.distill_fwd(p, None, fake, fake, None, fake, ws, None)
+    assert e.value.status == B.MLS_INVALID_ARG
+
+
+def test_backward_rejects_bad_arguments_before_device_work():
+    p = _fake_problem()
+    ws, st = B.query_sizes(p)
+    fake = 1 << 40
+    grads = [fake + (1 << 30) * (i + 1) for i in range(3)]
+    with pytest.raises(B.MlsError) as e:  # one coefficient vector without the other
+        B.distill_bwd(p, fake, fake + 256, None, grads, grads, fake + (1 << 20), ws, None)
+    assert e.value.status == B.MLS_INVALID_ARG
+    with pytest.raises(B.MlsError) as e:
+        B.distill_bwd(p, fake, None, None, grads, grads, fake + (1 << 20), 16, None)
+    assert e.value.status == B.MLS_WORKSPACE_TOO_SMALL
+
+
+def test_chunk_width_is_rounded():
+    p = _fake_problem(vocab_chunk=1000)
+    ws1, _ = B.query_sizes(p)
+    p2 = _fake_problem(vocab_chunk=1024)
+    ws2, _ = B.query_sizes(p2)
+    assert ws1 == ws2

@@ -1,0 +1,222 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 CPU oracle.
+
+Small cases run the whole oracle; they span several 128 x 128 tiles, ragged
+token and vocabulary tails, several backward vocabulary chunks, temperature,
+ignored labels, any teacher index, M = 1..4, V = 2 and T = 1. The benchmark
+workloads at full size are checked on sampled rows the oracle computes one by
+one, on a reduced-T instance for the head gradients, and through invariants
+that hold at any size.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_09703_amd import workloads as WL
+from tests.gpu_helpers import (assert_grad, assert_losses, assert_rows, rel_fro, run_gpu, to_np)
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _inputs(wl):
+    h, W, y = WL.make_inputs(wl, device=DEV)
+    return h, W, y, to_np(h), to_np(W), y.cpu().numpy()
+
+
+def _coeffs(M, teacher, alpha, tau, mode="paper"):
+    return oracle.coeffs(M, teacher, alpha=alpha, tau=tau, mode=mode)
+
+
+SMALL = [
+    # name, workload, teacher, alpha, mode, vocab_chunk
+    ("m3_ragged_tau1", WL.custom(3, 300, (64, 128, 192), 1000, ignore_frac=0.1, w_std=0.05, seed=1),
+     -1, 0.3, "paper", 512),
+    ("m3_tau2_teacher0", WL.custom(3, 260, (128, 64, 192), 1300, tau=2.0, w_std=0.08, seed=2),
+     0, 0.5, "paper", 256),
+    ("m4_peaky_ignore", WL.custom(4, 200, (64, 64, 128, 256), 777, w_std=0.02, w_scale=5.0,
+                                  ignore_frac=0.2, seed=3), -1, 1.0, "additive", 0),
+    ("m2_tau0p7_mid_teacher", WL.custom(2, 129, (256, 96), 2049, tau=0.7, w_std=0.1, seed=4),
+     0, 0.7, "paper", 1024),
+    ("m1_ce_only", WL.custom(1, 130, (96,), 300, w_std=0.1, seed=5), -1, 0.0, "paper", 0),
+    ("v2_binary", WL.custom(2, 64, (8, 16), 2, w_std=0.5, seed=6), -1, 0.5, "paper", 0),
+    ("t1_single_token", WL.custom(2, 1, (64, 64), 300, w_std=0.1, seed=7), -1, 0.5, "paper", 0),
+    ("c1_small_f32", WL.WORKLOADS["c1_small_f32"], -1, 1.0, "paper", 0),
+    ("f32_ragged", WL.custom(3, 150, (32, 36, 100), 555, dtype="f32", tau=1.5, w_std=0.1,
+                             ignore_frac=0.1, seed=8), -1, 0.4, "paper", 256),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_small_full_parity(case):
+    name, wl, teacher, alpha, mode, chunk = case
+    print(f"[parity] {name} M={wl.M} T={wl.T} V={wl.V} dims={wl.dims} {wl.dtype}", flush=True)
+    h, W, y, hn, Wn, yn = _inputs(wl)
+    g_ce, g_kl = _coeffs(wl.M, teacher, alpha, wl.tau, mode)
+    gpu = run_gpu(h, W, y, tau=wl.tau, teacher=teacher, g_ce=g_ce, g_kl=g_kl, vocab_chunk=chunk)
+    ref = oracle.forward(hn, Wn, yn, tau=wl.tau, teacher=teacher)
+    assert gpu["n_valid"] == ref["n_valid"]
+    assert gpu["flags"] == 0
+    assert_losses(gpu, ref, name)
+    assert_rows(gpu, ref, what=name)
+    gh, gW = oracle.backward(hn, Wn, yn, g_ce, g_kl, tau=wl.tau, teacher=teacher)
+    for i in range(wl.M):
+        e1 = assert_grad(gpu["grad_h"][i], gh[i], f"{name} grad_h[{i}]")
+        e2 = assert_grad(gpu["grad_W"][i], gW[i], f"{name} grad_W[{i}]")
+        # vocabulary tail (rows past the last multiple of 256)
+        tail = (wl.V // 256) * 256
+        if tail < wl.V:
+            assert_grad(gpu["grad_W"][i][tail:], gW[i][tail:], f"{name} grad_W[{i}] tail")
+        print(f"  sub-model {i}: grad_h err {e1:.2e}, grad_W err {e2:.2e}", flush=True)
+        ignored = yn == oracle.IGNORE_INDEX
+        assert np.all(gpu["grad_h"][i][ignored] == 0)
+
+
+def test_all_labels_ignored():
+    wl = WL.custom(2, 100, (64, 128), 500, w_std=0.1, seed=11, ignore_frac=1.0)
+    h, W, y, hn, Wn, yn = _inputs(wl)
+    assert (yn == -100).all()
+    gpu = run_gpu(h, W, y, g_ce=[1.0, 1.0], g_kl=[1.0, 0.0])
+    assert gpu["n_valid"] == 0
+    assert np.all(gpu["ce"] == 0) and np.all(gpu["kl"] == 0) and gpu["H"] == 0
+    for g in gpu["grad_h"] + gpu["grad_W"]:
+        assert np.all(g == 0)
+
+
+def test_identical_student_has_zero_kl():
+    wl = WL.custom(3, 256, (128, 64, 128), 3000, tau=1.7, w_std=0.1, seed=12)
+    h, W, y = WL.make_inputs(wl, device=DEV)
+    h[0] = h[2].clone()
+    W[0] = W[2].clone()
+    gpu = run_gpu(h, W, y, tau=wl.tau, g_ce=[0.0, 0.0, 0.0], g_kl=[1.0, 1.0, 0.0])
+    assert abs(gpu["kl"][0]) < 1e-5
+    assert gpu["kl"][1] > 1e-2
+    assert np.abs(gpu["kl_row"][0]).max() < 1e-5
+    assert np.abs(gpu["grad_h"][0]).max() <= 1e-7 * max(1.0, np.abs(gpu["grad_h"][1]).max())
+
+
+def test_uniform_logits_give_ln_v():
+    wl = WL.custom(2, 128, (64, 128), 5000, w_std=0.1, seed=13)
+    h, W, y = WL.make_inputs(wl, device=DEV)
+    W = [torch.zeros_like(x) for x in W]
+    gpu = run_gpu(h, W, y, grads=False)
+    np.testing.assert_allclose(gpu["ce"], np.log(5000.0), rtol=1e-6)
+    assert np.abs(gpu["kl"]).max() < 1e-6
+
+
+def test_out_of_range_label_is_flagged_and_ignored():
+    wl = WL.custom(2, 128, (64, 64), 700, w_std=0.1, seed=14)
+    h, W, y = WL.make_inputs(wl, device=DEV)
+    y[5] = 700
+    y[9] = -7
+    gpu = run_gpu(h, W, y, g_ce=[1.0, 1.0], g_kl=[0.5, 0.0])
+    assert gpu["flags"] == 1
+    assert gpu["n_valid"] == 126
+    assert np.all(gpu["grad_h"][0][[5, 9]] == 0)
+
+
+def test_deterministic_bitwise():
+    wl = WL.custom(3, 384, (128, 256, 384), 4000, tau=1.3, ignore_frac=0.05, seed=15)
+    h, W, y = WL.make_inputs(wl, device=DEV)
+    g_ce, g_kl = _coeffs(3, -1, 0.3, wl.tau)
+    a = run_gpu(h, W, y, tau=wl.tau, g_ce=g_ce, g_kl=g_kl, vocab_chunk=1024)
+    b = run_gpu(h, W, y, tau=wl.tau, g_ce=g_ce, g_kl=g_kl, vocab_chunk=1024)
+    for k in ("ce", "kl", "lse1", "lset", "kl_row"):
+        assert np.array_equal(a[k], b[k]), k
+    for i in range(3):
+        assert np.array_equal(a["grad_h"][i], b["grad_h"][i])
+        assert np.array_equal(a["grad_W"][i], b["grad_W"][i])
+
+
+def test_default_coefficients_follow_alpha():
+    """With no coefficient vectors the library uses eq. (3) with the problem's alpha and tau."""
+    wl = WL.custom(3, 200, (64, 128, 128), 900, tau=2.0, w_std=0.1, seed=16)
+    h, W, y, hn, Wn, yn = _inputs(wl)
+    gpu = run_gpu(h, W, y, tau=2.0, alpha=0.25)
+    g_ce, g_kl = oracle.coeffs(3, -1, alpha=0.25, tau=2.0)
+    gh, gW = oracle.backward(hn, Wn, yn, g_ce, g_kl, tau=2.0)
+    for i in range(3):
+        assert_grad(gpu["grad_h"][i], gh[i], f"grad_h[{i}]")
+        assert_grad(gpu["grad_W"][i], gW[i], f"grad_W[{i}]")
+
+
+def test_autograd_front_end():
+    from paper_2608_09703_amd import distill
+    wl = WL.custom(3, 256, (64, 128, 192), 1500, tau=1.5, w_std=0.1, ignore_frac=0.1, seed=17)
+    h, W, y, hn, Wn, yn = _inputs(wl)
+    hs = [x.clone().requires_grad_(True) for x in h]
+    Ws = [x.clone().requires_grad_(True) for x in W]
+    ce, kl, H = distill(hs, Ws, y, tau=1.5)
+    w = torch.tensor([0.5, 1.0, 2.0], device=DEV)
+    alpha = 0.3
+    loss = (w * ((1 - alpha) * ce + alpha * 1.5 ** 2 * kl)).sum()
+    loss = loss + 0.5 * ce[2]  # extra teacher weight: any linear objective works
+    loss.backward()
+    g_ce = np.array([0.5 * 0.7, 1.0 * 0.7, 2.0 * 0.7 + 0.5])
+    g_kl = np.array([0.5 * 0.3 * 2.25, 1.0 * 0.3 * 2.25, 2.0 * 0.3 * 2.25])
+    ref = oracle.forward(hn, Wn, yn, tau=1.5)
+    np.testing.assert_allclose(ce.detach().cpu().numpy(), ref["ce"], rtol=1e-3)
+    np.testing.assert_allclose(kl.detach().cpu().numpy()[:2], ref["kl"][:2], rtol=1e-3)
+    gh, gW = oracle.backward(hn, Wn, yn, g_ce, g_kl, tau=1.5)
+    for i in range(3):
+        assert_grad(hs[i].grad.float().cpu().numpy(), gh[i], f"grad_h[{i}]")
+        assert_grad(Ws[i].grad.float().cpu().numpy(), gW[i], f"grad_W[{i}]")
+
+
+# ---------------------------------------------------------------------------
+# benchmark workloads at full size
+# ---------------------------------------------------------------------------
+
+FULL = ["c2_m3_v50k", "c3_m3_v128k_tau2", "c4_m4_v128k_peaky"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_sampled_rows(name):
+    wl = WL.WORKLOADS[name]
+    print(f"[parity-full] {name} M={wl.M} T={wl.T} V={wl.V} dims={wl.dims}", flush=True)
+    h, W, y = WL.make_inputs(wl, device=DEV)
+    g_ce, g_kl = _coeffs(wl.M, -1, wl.alpha, wl.tau)
+    gpu = run_gpu(h, W, y, tau=wl.tau, g_ce=g_ce, g_kl=g_kl)
+    hn, Wn, yn = to_np(h), to_np(W), y.cpu().numpy()
+    del h, W
+    rng = np.random.default_rng(wl.seed + 7)
+    rows = np.sort(rng.choice(wl.T, size=96, replace=False))
+    ref = oracle.per_row(hn, Wn, yn, rows, tau=wl.tau)
+    assert_rows(gpu, ref, rows=rows, what=name)
+    N = int((yn != -100).sum())
+    assert gpu["n_valid"] == N
+    # the means are the means of the per-row values
+    for i in range(wl.M):
+        np.testing.assert_allclose(gpu["ce"][i], gpu["ce_row"][i].astype(np.float64).sum() / N,
+                                   rtol=1e-5)
+    ghr = oracle.grad_h_rows(hn, Wn, yn, rows[:32], g_ce, g_kl, tau=wl.tau)
+    for i in range(wl.M):
+        assert_grad(gpu["grad_h"][i][rows[:32]], ghr[i], f"{name} grad_h[{i}] rows")
+        # every row of the logit gradient sums to zero: sum_v grad_W = 0
+        colsum = gpu["grad_W"][i].astype(np.float64).sum(axis=0)
+        scale = np.abs(gpu["grad_W"][i]).astype(np.float64).sum(axis=0).max()
+        assert np.abs(colsum).max() <= 1e-3 * scale
+        ign = yn == -100
+        if ign.any():
+            assert np.all(gpu["grad_h"][i][ign] == 0)
+
+
+@pytest.mark.parametrize("name", ["c2_m3_v50k", "c3_m3_v128k_tau2"])
+def test_reduced_T_full_head_gradient(name):
+    """Same V, widths and distributions with T = 512: every grad_W element checked."""
+    wl = WL.WORKLOADS[name].replace(T=512)
+    print(f"[parity-reducedT] {name} T={wl.T} V={wl.V}", flush=True)
+    h, W, y, hn, Wn, yn = _inputs(wl)
+    g_ce, g_kl = _coeffs(wl.M, -1, wl.alpha, wl.tau)
+    gpu = run_gpu(h, W, y, tau=wl.tau, g_ce=g_ce, g_kl=g_kl)
+    ref = oracle.forward(hn, Wn, yn, tau=wl.tau)
+    assert_losses(gpu, ref, name)
+    gh, gW = oracle.backward(hn, Wn, yn, g_ce, g_kl, tau=wl.tau)
+    for i in range(wl.M):
+        assert_grad(gpu["grad_h"][i], gh[i], f"{name} grad_h[{i}]")
+        assert_grad(gpu["grad_W"][i], gW[i], f"{name} grad_W[{i}]")
+        tail = (wl.V // 256) * 256
+        if tail < wl.V:
+            assert_grad(gpu["grad_W"][i][tail:], gW[i][tail:], f"{name} grad_W[{i}] tail")
