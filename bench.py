@@ -93,7 +93,7 @@ def main():
 
     import torch
     from paper_2608_09703_amd import binding as B
-    from paper_2608_09703_amd import distill as D
+    from paper_2608_09703_amd import api as D
     from paper_2608_09703_amd import workloads as WL
 
     name = args.workload or WL.HEADLINE

@@ -6,14 +6,14 @@ package does not load the library: :func:`distill` and the wrappers in
 :mod:`.binding` load it on first use and raise if it is missing.
 """
 
-__all__ = ["distill", "binding", "workloads"]
+__all__ = ["distill", "api", "binding", "workloads"]
 
 
 def __getattr__(name):
     if name == "distill":
-        from .distill import distill
+        from .api import distill
         return distill
-    if name in ("binding", "workloads"):
+    if name in ("api", "binding", "workloads"):
         import importlib
         return importlib.import_module(f".{name}", __name__)
     raise AttributeError(name)

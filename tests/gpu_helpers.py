@@ -6,7 +6,7 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from paper_2608_09703_amd import distill as D
+from paper_2608_09703_amd import api as D
 
 LOSS_RTOL = 1e-3     # losses: relative 1e-3 ...
 LOSS_ATOL = 1e-5     # ... with an absolute floor for values near 0 (KL of equal models)

@@ -143,7 +143,7 @@ def test_default_coefficients_follow_alpha():
 
 
 def test_autograd_front_end():
-    from paper_2608_09703_amd import distill
+    from paper_2608_09703_amd.api import distill
     wl = WL.custom(3, 256, (64, 128, 192), 1500, tau=1.5, w_std=0.1, ignore_frac=0.1, seed=17)
     h, W, y, hn, Wn, yn = _inputs(wl)
     hs = [x.clone().requires_grad_(True) for x in h]
