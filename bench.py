@@ -66,13 +66,17 @@ def cpu_baseline(wl, h, W, y, g_ce, g_kl, rows_req):
 
     if rows_req > 0:
         rows = rows_req
+        dt = run(rows)
     else:
-        probe = 16
-        tp = run(probe)
-        rows = int(min(wl.T, max(probe, probe * 15.0 / max(tp, 1e-3))))
-        rows = max(16, rows // 16 * 16)
-        log(f"oracle probe: {probe} rows in {tp:.2f}s -> sample {rows} rows")
-    dt = run(rows)
+        # grow the sample until one timed run costs 10-30 s of host time
+        rows = 32
+        while True:
+            dt = run(rows)
+            log(f"oracle sample {rows} rows: {dt:.1f} s")
+            if dt >= 10.0 or rows >= wl.T:
+                break
+            rows = int(min(wl.T, max(2 * rows, rows * 14.0 / max(dt, 1e-3))))
+            rows = max(16, rows // 16 * 16)
     return {
         "value": rows / dt,
         "unit": "tokens/s",

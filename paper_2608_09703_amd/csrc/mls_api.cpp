@@ -88,6 +88,7 @@ struct Plan {
   int M = 0;
   int s = 0;
   bool f32 = false;
+  bool wide = false;  // wide bf16 tile core (every width a multiple of 64)
   int es = 2;
   int64_t T = 0, V = 0;
   int64_t sumd = 0;
@@ -144,9 +145,12 @@ void make_plan(const mls_problem* p, Plan& pl) {
   pl.V = p->V;
   pl.sumd = 0;
   for (int i = 0; i < p->M; ++i) pl.sumd += p->d[i];
+  pl.wide = !pl.f32;
+  for (int i = 0; i < p->M; ++i) pl.wide = pl.wide && (p->d[i] % 64 == 0);
   pl.T_pad = round_up(p->T, kFusedBN);
   pl.n_tt = (int)(pl.T_pad / kFusedBN);
-  pl.n_vt_fwd = (int)((p->V + kFusedBM - 1) / kFusedBM);
+  const int fbm = fused_tile_rows(pl.wide);
+  pl.n_vt_fwd = (int)((p->V + fbm - 1) / fbm);
   const int64_t vmax = round_up(p->V, 256);
   int64_t vc;
   if (p->vocab_chunk > 0) {
@@ -206,6 +210,7 @@ void fill_common(const mls_problem* p, const Plan& pl, FusedArgs& a) {
   a.ignore_index = p->ignore_index;
   a.tau = p->tau;
   a.inv_tau = 1.0f / p->tau;
+  a.wide = pl.wide ? 1 : 0;
   a.n_tt = pl.n_tt;
   a.T_pad = pl.T_pad;
   a.Vc = pl.Vc;
@@ -371,7 +376,7 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
 
   FusedArgs a;
   fill_common(p, pl, a);
-  a.n_vt = (int)(pl.Vc / kFusedBM);
+  a.n_vt = (int)(pl.Vc / fused_tile_rows(pl.wide));
   a.lse1 = sf;
   a.lset = sf + (int64_t)pl.M * pl.T;
   a.n_valid = reinterpret_cast<const int32_t*>(static_cast<const char*>(stats) + pl.header_off);
@@ -390,6 +395,8 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
     acc += p->d[i];
   }
   const size_t slab_stride = (size_t)pl.T_pad * pl.Vc * pl.es;
+  const int tbm = gemm_tile_rows(pl.f32);
+  const int tbn = gemm_tile_cols(pl.f32);
   hipError_t e;
 
   // h_i^T [d_i, T_pad] for the grad_W products
@@ -467,8 +474,8 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
       g.ldc = p->d[i];
       g.rows = vrows;
       g.cols = p->d[i];
-      g.tiles_m = (int)((vrows + kGemmBM - 1) / kGemmBM);
-      g.tiles_n = (int)((p->d[i] + kGemmBN - 1) / kGemmBN);
+      g.tiles_m = (int)((vrows + tbm - 1) / tbm);
+      g.tiles_n = (int)((p->d[i] + tbn - 1) / tbn);
       g.tile_begin = tiles;
       g.accumulate = (p->flags & MLS_ACCUMULATE_GRAD_W) ? 1 : 0;
       tiles += g.tiles_m * g.tiles_n;
@@ -495,8 +502,8 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
       g.ldc = p->d[i];
       g.rows = pl.T;
       g.cols = p->d[i];
-      g.tiles_m = (int)((pl.T + kGemmBM - 1) / kGemmBM);
-      g.tiles_n = (int)((p->d[i] + kGemmBN - 1) / kGemmBN);
+      g.tiles_m = (int)((pl.T + tbm - 1) / tbm);
+      g.tiles_n = (int)((p->d[i] + tbn - 1) / tbn);
       g.tile_begin = tiles;
       g.accumulate = (c > 0 || (p->flags & MLS_ACCUMULATE_GRAD_H)) ? 1 : 0;
       tiles += g.tiles_m * g.tiles_n;

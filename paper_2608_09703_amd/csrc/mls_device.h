@@ -113,6 +113,11 @@ struct TileLoader {
 template <typename E, int BM, int BN, int WGM, int WGN>
 struct TileMma {
   static_assert(WGM * WGN == 4, "four waves per block");
+  static constexpr int kBM = BM;
+  static constexpr int kBN = BN;
+  static constexpr int kWGM = WGM;
+  static constexpr int kWGN = WGN;
+  static constexpr int NT = kThreads;
   static constexpr int WTM = BM / WGM;
   static constexpr int WTN = BN / WGN;
   static constexpr int FM = WTM / 32;

@@ -18,6 +18,7 @@
 // to the chunk slab in two layouts for the two backward GEMMs.
 #include <math.h>
 
+#include "mls_core.h"
 #include "mls_device.h"
 #include "mls_launch.h"
 
@@ -25,14 +26,46 @@ namespace mls {
 
 namespace {
 
-constexpr int BM = kFusedBM;
-constexpr int BN = kFusedBN;
-constexpr int WGM = 2;
-constexpr int WGN = 2;
+// Tile cores: the general one (any width, fp32 or bf16) and the wide bf16 one
+// (widths multiples of 64).
+using GenMmaBf16 = TileMma<Bf16, kFusedBM, kFusedBN, 2, 2>;
+using GenMmaF32 = TileMma<F32, kFusedBM, kFusedBN, 2, 2>;
+using WideFused = WideMma<kFusedWideBM, kFusedBN, 2, 2, 2>;
 
-template <typename E, bool TAU1>
-__global__ __launch_bounds__(kThreads, 2) void fused_fwd_kernel(FusedArgs a) {
-  using Mma = TileMma<E, BM, BN, WGM, WGN>;
+// Per-lane copy of the teacher's tile values (its softmax weights), laid out
+// like the accumulators. The bf16 paths keep them as packed bf16 pairs
+// (half the registers; 2^-9 relative rounding), the fp32 path in fp32.
+template <int FM, int FN, bool PACK>
+struct TeacherTile;
+
+template <int FM, int FN>
+struct TeacherTile<FM, FN, false> {
+  float v[FM][FN][16];
+  __device__ __forceinline__ void set(int fm, int fn, int r, float x) { v[fm][fn][r] = x; }
+  __device__ __forceinline__ float get(int fm, int fn, int r) const { return v[fm][fn][r]; }
+};
+
+template <int FM, int FN>
+struct TeacherTile<FM, FN, true> {
+  uint32_t v[FM][FN][8];
+  __device__ __forceinline__ void set(int fm, int fn, int r, float x) {
+    const uint32_t b = to_storage<Bf16>(x);
+    if (r & 1)
+      v[fm][fn][r >> 1] = (v[fm][fn][r >> 1] & 0xffffu) | (b << 16);
+    else
+      v[fm][fn][r >> 1] = b;
+  }
+  __device__ __forceinline__ float get(int fm, int fn, int r) const {
+    const uint32_t w = v[fm][fn][r >> 1];
+    return __uint_as_float((r & 1) ? (w & 0xffff0000u) : (w << 16));
+  }
+};
+
+template <class Mma, typename E, bool TAU1, int MINB = 1>
+__global__ __launch_bounds__(Mma::NT, MINB) void fused_fwd_kernel(FusedArgs a) {
+  constexpr int BM = Mma::kBM;
+  constexpr int BN = Mma::kBN;
+  constexpr int WGM = Mma::kWGM;
   constexpr int FM = Mma::FM;
   constexpr int FN = Mma::FN;
   __shared__ __attribute__((aligned(16))) char smem[Mma::kSmemBytes];
@@ -44,14 +77,16 @@ __global__ __launch_bounds__(kThreads, 2) void fused_fwd_kernel(FusedArgs a) {
   const int wm = wave % WGM;
   const int wn = wave / WGM;
   const int hi = lane >> 5;
-  const int tt = blockIdx.x % a.n_tt;
-  const int vt = blockIdx.x / a.n_tt;
+  const int bl = xcd_remap(blockIdx.x, gridDim.x);
+  const int tt = bl % a.n_tt;
+  const int vt = bl / a.n_tt;
   const int64_t vbase = (int64_t)vt * BM;
   const int64_t tbase = (int64_t)tt * BN;
   const bool full = vbase + BM <= a.V;
   const float ct = kLog2e * a.inv_tau;
 
-  float e_t[FM][FN][16];  // teacher weights exp((l_s - max_s) / tau); 0 outside V
+  // teacher weights exp((l_s - max_s) / tau); 0 outside V
+  TeacherTile<FM, FN, false> e_t;
   Mma mma;
 
   for (int oi = 0; oi < a.M; ++oi) {
@@ -98,7 +133,7 @@ __global__ __launch_bounds__(kThreads, 2) void fused_fwd_kernel(FusedArgs a) {
             const float l = mma.acc[fm][fn][r];
             const float x = l - mb[fn];
             const float e = ok ? fast_exp2(x * ct) : 0.f;
-            e_t[fm][fn][r] = e;
+            e_t.set(fm, fn, r, e);
             st += e;
             xr = fmaf(e, l, xr);
             if (!TAU1) s1 += ok ? fast_exp2(x * kLog2e) : 0.f;
@@ -114,7 +149,7 @@ __global__ __launch_bounds__(kThreads, 2) void fused_fwd_kernel(FusedArgs a) {
             const float x = l - mb[fn];
             s1 += ok ? fast_exp2(x * kLog2e) : 0.f;
             if (!TAU1) st += ok ? fast_exp2(x * ct) : 0.f;
-            xr = fmaf(e_t[fm][fn][r], l, xr);
+            xr = fmaf(e_t.get(fm, fn, r), l, xr);
           }
         if (TAU1) st = s1;
       }
@@ -165,9 +200,11 @@ __device__ __forceinline__ void store4<F32>(float* p, float a0, float a1, float 
   *reinterpret_cast<float4*>(p) = make_float4(a0, a1, a2, a3);
 }
 
-template <typename E, bool TAU1>
-__global__ __launch_bounds__(kThreads, 1) void fused_bwd_kernel(FusedArgs a) {
-  using Mma = TileMma<E, BM, BN, WGM, WGN>;
+template <class Mma, typename E, bool TAU1>
+__global__ __launch_bounds__(Mma::NT, 1) void fused_bwd_kernel(FusedArgs a) {
+  constexpr int BM = Mma::kBM;
+  constexpr int BN = Mma::kBN;
+  constexpr int WGM = Mma::kWGM;
   using S = typename E::storage;
   constexpr int FM = Mma::FM;
   constexpr int FN = Mma::FN;
@@ -178,8 +215,9 @@ __global__ __launch_bounds__(kThreads, 1) void fused_bwd_kernel(FusedArgs a) {
   const int wave = tid >> 6;
   const int wm = wave % WGM;
   const int wn = wave / WGM;
-  const int tt = blockIdx.x % a.n_tt;
-  const int vt = blockIdx.x / a.n_tt;
+  const int bl = xcd_remap(blockIdx.x, gridDim.x);
+  const int tt = bl % a.n_tt;
+  const int vt = bl / a.n_tt;
   const int64_t vloc = (int64_t)vt * BM;  // row offset inside the chunk
   const int64_t vbase = a.v0 + vloc;      // absolute vocabulary row
   const int64_t tbase = (int64_t)tt * BN;
@@ -200,7 +238,8 @@ __global__ __launch_bounds__(kThreads, 1) void fused_bwd_kernel(FusedArgs a) {
     ylab[fn] = (rv[fn] && rel >= 0 && rel < BM) ? (int)rel : -1;
   }
 
-  float q_t[FM][FN][16];  // teacher softmax at tau; 0 outside V and on invalid rows
+  // teacher softmax at tau; 0 outside V and on invalid rows
+  TeacherTile<FM, FN, E::kBytes == 2> q_t;
   Mma mma;
 
   for (int oi = 0; oi < a.M; ++oi) {
@@ -238,13 +277,13 @@ __global__ __launch_bounds__(kThreads, 1) void fused_bwd_kernel(FusedArgs a) {
             const float oh = row == ylab[fn] ? 1.f : 0.f;
             if (oi == 0) {
               const float q = ok ? fast_exp2(fmaf(l, ct, -lts)) : 0.f;
-              q_t[fm][fn][r] = q;
+              q_t.set(fm, fn, r, q);
               const float p1 = TAU1 ? q : (ok ? fast_exp2(fmaf(l, kLog2e, -l1s)) : 0.f);
               g[rr] = cg * (p1 - oh);
             } else {
               const float p1 = ok ? fast_exp2(fmaf(l, kLog2e, -l1s)) : 0.f;
               const float pt = TAU1 ? p1 : (ok ? fast_exp2(fmaf(l, ct, -lts)) : 0.f);
-              g[rr] = fmaf(cg, p1 - oh, ck * (pt - q_t[fm][fn][r]));
+              g[rr] = fmaf(cg, p1 - oh, ck * (pt - q_t.get(fm, fn, r)));
             }
           }
           const int row0 = Mma::row_of(wm, fm, rg * 4, lane);
@@ -257,32 +296,197 @@ __global__ __launch_bounds__(kThreads, 1) void fused_bwd_kernel(FusedArgs a) {
   }
 }
 
-template <typename E, bool TAU1>
+// Backward tile kernel of the wide bf16 core. Same arithmetic as
+// fused_bwd_kernel; the bf16 logit-gradient tile is staged in LDS as
+// [token][vocabulary] (rows of 512 bytes, 16-byte chunks XOR-swizzled with the
+// token index) and leaves the block as 16-byte coalesced stores: token-major
+// rows by plain copies, vocabulary-major rows through transposing LDS reads
+// (ds_read_b64_tr_b16: within a 16-lane group, lane j addresses row k0 + j/4,
+// column n0 + 4 (j % 4); lane i receives column n0 + i of rows k0 .. k0 + 3).
+template <bool TAU1>
+__global__ __launch_bounds__(256, 1) void fused_bwd_wide_kernel(FusedArgs a) {
+  using Mma = WideFused;
+  constexpr int BM = Mma::kBM;  // 256 vocabulary rows
+  constexpr int BN = Mma::kBN;  // 128 tokens
+  constexpr int WGM = Mma::kWGM;
+  constexpr int FM = Mma::FM;
+  constexpr int FN = Mma::FN;
+  constexpr int kGRow = BM * 2;  // bytes per token row of the staged tile
+  static_assert(BN * kGRow <= Mma::kSmemBytes, "staged tile fits in the stage memory");
+  typedef short v4s_t __attribute__((ext_vector_type(4)));
+  __shared__ __attribute__((aligned(16))) char smem[Mma::kSmemBytes];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave % WGM;
+  const int wn = wave / WGM;
+  const int bl = xcd_remap(blockIdx.x, gridDim.x);
+  const int tt = bl % a.n_tt;
+  const int vt = bl / a.n_tt;
+  const int64_t vloc = (int64_t)vt * BM;
+  const int64_t vbase = a.v0 + vloc;
+  const int64_t tbase = (int64_t)tt * BN;
+  const bool full = vbase + BM <= a.V;
+  const int nv = *a.n_valid;
+  const float invN = nv > 0 ? 1.0f / (float)nv : 0.0f;
+  const float ct = kLog2e * a.inv_tau;
+
+  int tcol[FN];
+  int ylab[FN];
+  bool rv[FN];
+#pragma unroll
+  for (int fn = 0; fn < FN; ++fn) {
+    tcol[fn] = Mma::col_of(wn, fn, lane);
+    const int64_t t = tbase + tcol[fn];
+    const int64_t y = t < a.T ? a.labels[t] : a.ignore_index;
+    rv[fn] = t < a.T && y != a.ignore_index && y >= 0 && y < a.V;
+    const int64_t rel = y - vbase;
+    ylab[fn] = (rv[fn] && rel >= 0 && rel < BM) ? (int)rel : -1;
+  }
+
+  TeacherTile<FM, FN, true> q_t;
+  Mma mma;
+
+  for (int oi = 0; oi < a.M; ++oi) {
+    const int i = a.order[oi];
+    const int64_t kb = a.d[i] * 2;
+    mma.run(static_cast<const char*>(a.W[i]), kb, vbase, a.V, static_cast<const char*>(a.h[i]),
+            kb, tbase, a.T, kb, smem, tid);
+    const float gce = a.g_ce ? a.g_ce[i] : a.host_gce[i];
+    const float gkl = a.g_kl ? a.g_kl[i] : a.host_gkl[i];
+
+    // 1. logit gradient -> bf16 tile in LDS
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      const int64_t t = tbase + tcol[fn];
+      const float l1 = rv[fn] ? a.lse1[(int64_t)i * a.T + t] : INFINITY;
+      const float lt = rv[fn] ? a.lset[(int64_t)i * a.T + t] : INFINITY;
+      const float cg = rv[fn] ? gce * invN : 0.f;
+      const float ck = (rv[fn] && oi != 0) ? gkl * invN * a.inv_tau : 0.f;
+      const float l1s = l1 * kLog2e;
+      const float lts = lt * kLog2e;
+      const int trow = tcol[fn];
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+          float g[4];
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) {
+            const int r = rg * 4 + rr;
+            const int row = Mma::row_of(wm, fm, r, lane);
+            const bool ok = full || vbase + row < a.V;
+            const float l = mma.acc[fm][fn][r];
+            const float oh = row == ylab[fn] ? 1.f : 0.f;
+            if (oi == 0) {
+              const float q = ok ? fast_exp2(fmaf(l, ct, -lts)) : 0.f;
+              q_t.set(fm, fn, r, q);
+              const float p1 = TAU1 ? q : (ok ? fast_exp2(fmaf(l, kLog2e, -l1s)) : 0.f);
+              g[rr] = cg * (p1 - oh);
+            } else {
+              const float p1 = ok ? fast_exp2(fmaf(l, kLog2e, -l1s)) : 0.f;
+              const float pt = TAU1 ? p1 : (ok ? fast_exp2(fmaf(l, ct, -lts)) : 0.f);
+              g[rr] = fmaf(cg, p1 - oh, ck * (pt - q_t.get(fm, fn, r)));
+            }
+          }
+          const int v0 = Mma::row_of(wm, fm, rg * 4, lane);  // multiple of 4
+          uint2 w;
+          w.x = (uint32_t)to_storage<Bf16>(g[0]) | ((uint32_t)to_storage<Bf16>(g[1]) << 16);
+          w.y = (uint32_t)to_storage<Bf16>(g[2]) | ((uint32_t)to_storage<Bf16>(g[3]) << 16);
+          const int off = trow * kGRow + ((((v0 >> 3) ^ (trow & 31))) << 4) + ((v0 >> 2) & 1) * 8;
+          *reinterpret_cast<uint2*>(smem + off) = w;
+          __builtin_amdgcn_sched_barrier(0);  // bound live ranges: one 4-row group at a time
+        }
+    }
+    block_barrier();
+
+    // 2. token-major slab: 128 rows x 32 chunks of 16 bytes
+    uint16_t* slab = static_cast<uint16_t*>(a.slab) + (int64_t)i * a.T_pad * a.Vc;
+    uint16_t* slabT = static_cast<uint16_t*>(a.slabT) + (int64_t)i * a.T_pad * a.Vc;
+#pragma unroll 4
+    for (int j = 0; j < BN * 32 / 256; ++j) {
+      const int idx = tid + 256 * j;
+      const int t = idx >> 5;
+      const int c = idx & 31;
+      const uint4 v = *reinterpret_cast<const uint4*>(smem + t * kGRow + ((c ^ (t & 31)) << 4));
+      *reinterpret_cast<uint4*>(slab + (tbase + t) * a.Vc + vloc + c * 8) = v;
+    }
+    // 3. vocabulary-major slab: 256 rows x 16 chunks of 8 tokens, via transposing reads
+    {
+      const int grp = lane >> 4;
+      const int j16 = lane & 15;
+#pragma unroll 2
+      for (int it = 0; it < (BM / 16) * (BN / 8) / 16; ++it) {
+        const int task = (it * 4 + wave) * 4 + grp;
+        const int vb = (task % (BM / 16)) * 16;
+        const int k0 = (task / (BM / 16)) * 8;
+        const int vv = vb + 4 * (j16 & 3);
+        const int ta = k0 + (j16 >> 2);
+        const int tb = ta + 4;
+        const int oa = ta * kGRow + (((vv >> 3) ^ (ta & 31)) << 4) + (vv & 7) * 2;
+        const int ob = tb * kGRow + (((vv >> 3) ^ (tb & 31)) << 4) + (vv & 7) * 2;
+        const v4s_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) v4s_t*)((__attribute__((address_space(3))) char*)smem + oa));
+        const v4s_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) v4s_t*)((__attribute__((address_space(3))) char*)smem + ob));
+        uint4 o;
+        o.x = (uint32_t)(uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16);
+        o.y = (uint32_t)(uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16);
+        o.z = (uint32_t)(uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16);
+        o.w = (uint32_t)(uint16_t)hi[2] | ((uint32_t)(uint16_t)hi[3] << 16);
+        *reinterpret_cast<uint4*>(slabT + (vloc + vb + j16) * a.T_pad + tbase + k0) = o;
+      }
+    }
+    block_barrier();  // the stage memory is reused by the next tile product
+  }
+}
+
+template <class Mma, typename E, bool TAU1>
 hipError_t launch_fwd_t(const FusedArgs& a, hipStream_t stream) {
   dim3 grid((unsigned)a.n_tt * (unsigned)a.n_vt);
-  hipLaunchKernelGGL((fused_fwd_kernel<E, TAU1>), grid, dim3(kThreads), 0, stream, a);
+  hipLaunchKernelGGL((fused_fwd_kernel<Mma, E, TAU1>), grid, dim3(Mma::NT), 0, stream, a);
   return hipGetLastError();
 }
 
-template <typename E, bool TAU1>
+template <class Mma, typename E, bool TAU1>
 hipError_t launch_bwd_t(const FusedArgs& a, hipStream_t stream) {
   dim3 grid((unsigned)a.n_tt * (unsigned)a.n_vt);
-  hipLaunchKernelGGL((fused_bwd_kernel<E, TAU1>), grid, dim3(kThreads), 0, stream, a);
+  hipLaunchKernelGGL((fused_bwd_kernel<Mma, E, TAU1>), grid, dim3(Mma::NT), 0, stream, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
+int fused_tile_rows(bool wide) { return wide ? kFusedWideBM : kFusedBM; }
+
 hipError_t launch_fused_fwd(const FusedArgs& a, bool f32, hipStream_t stream) {
   const bool tau1 = a.tau == 1.0f;
-  if (f32) return tau1 ? launch_fwd_t<F32, true>(a, stream) : launch_fwd_t<F32, false>(a, stream);
-  return tau1 ? launch_fwd_t<Bf16, true>(a, stream) : launch_fwd_t<Bf16, false>(a, stream);
+  if (f32)
+    return tau1 ? launch_fwd_t<GenMmaF32, F32, true>(a, stream)
+                : launch_fwd_t<GenMmaF32, F32, false>(a, stream);
+  if (a.wide)
+    return tau1 ? launch_fwd_t<WideFused, Bf16, true>(a, stream)
+                : launch_fwd_t<WideFused, Bf16, false>(a, stream);
+  return tau1 ? launch_fwd_t<GenMmaBf16, Bf16, true>(a, stream)
+              : launch_fwd_t<GenMmaBf16, Bf16, false>(a, stream);
 }
 
 hipError_t launch_fused_bwd(const FusedArgs& a, bool f32, hipStream_t stream) {
   const bool tau1 = a.tau == 1.0f;
-  if (f32) return tau1 ? launch_bwd_t<F32, true>(a, stream) : launch_bwd_t<F32, false>(a, stream);
-  return tau1 ? launch_bwd_t<Bf16, true>(a, stream) : launch_bwd_t<Bf16, false>(a, stream);
+  if (f32)
+    return tau1 ? launch_bwd_t<GenMmaF32, F32, true>(a, stream)
+                : launch_bwd_t<GenMmaF32, F32, false>(a, stream);
+  if (a.wide) {
+    dim3 grid((unsigned)a.n_tt * (unsigned)a.n_vt);
+    if (tau1)
+      hipLaunchKernelGGL(fused_bwd_wide_kernel<true>, grid, dim3(WideFused::NT), 0, stream, a);
+    else
+      hipLaunchKernelGGL(fused_bwd_wide_kernel<false>, grid, dim3(WideFused::NT), 0, stream, a);
+    return hipGetLastError();
+  }
+  return tau1 ? launch_bwd_t<GenMmaBf16, Bf16, true>(a, stream)
+              : launch_bwd_t<GenMmaBf16, Bf16, false>(a, stream);
 }
 
 }  // namespace mls

@@ -5,6 +5,7 @@
 //   grad_h_i       += G_i W_i[chunk]  A = G_i slab   [T_pad, Vc], B = W_i[chunk]^T [d_i, Vc]
 // Both are NT tile products on the shared MFMA main loop; the transposed
 // operands h_i^T and W_i[chunk]^T are produced by the transpose kernel below.
+#include "mls_core.h"
 #include "mls_device.h"
 #include "mls_launch.h"
 
@@ -56,6 +57,54 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_nt_kernel(GemmArgs a) {
     }
 }
 
+// bf16 path: 256 x 256 tiles, 8 waves (2 per SIMD), direct-to-LDS loads; K is a
+// multiple of 64 (the callers pad it).
+constexpr int kWideBM = 256;
+constexpr int kWideBN = 256;
+constexpr int kWideThreads = 512;
+
+__global__ __launch_bounds__(kWideThreads, 2) void gemm_wide_kernel(GemmArgs a, int nb) {
+  using Mma = WideMma<kWideBM, kWideBN, 2, 4, 2>;
+  constexpr int FM = Mma::FM;
+  constexpr int FN = Mma::FN;
+  __shared__ __attribute__((aligned(16))) char smem[Mma::kSmemBytes];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave % 2;
+  const int wn = wave / 2;
+  const int b = xcd_remap(blockIdx.x, nb);
+  int gi = 0;
+  for (int k = 1; k < a.ngroups; ++k)
+    if (b >= a.g[k].tile_begin) gi = k;
+  const GemmGroup& g = a.g[gi];
+  const int local = b - g.tile_begin;
+  const int tn = local % g.tiles_n;
+  const int tm = local / g.tiles_n;
+  const int64_t m0 = (int64_t)tm * kWideBM;
+  const int64_t n0 = (int64_t)tn * kWideBN;
+
+  Mma mma;
+  mma.run(static_cast<const char*>(g.A), g.lda * 2, m0, g.rows, static_cast<const char*>(g.B),
+          g.ldb * 2, n0, g.cols, a.K * 2, smem, tid);
+
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      const int64_t n = n0 + Mma::col_of(wn, fn, lane);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t m = m0 + Mma::row_of(wm, fm, r, lane);
+        if (m < g.rows && n < g.cols) {
+          float* c = g.C + m * g.ldc + n;
+          *c = g.accumulate ? *c + mma.acc[fm][fn][r] : mma.acc[fm][fn][r];
+        }
+      }
+    }
+}
+
 template <typename S>
 __global__ __launch_bounds__(kThreads) void transpose_kernel(TransposeArgs a) {
   const TransposeJob& j = a.j[blockIdx.z];
@@ -84,8 +133,16 @@ __global__ __launch_bounds__(kThreads) void transpose_kernel(TransposeArgs a) {
 
 }  // namespace
 
+int gemm_tile_rows(bool f32) { return f32 ? kGemmBM : kWideBM; }
+int gemm_tile_cols(bool f32) { return f32 ? kGemmBN : kWideBN; }
+
 hipError_t launch_gemm_nt(const GemmArgs& a, int total_tiles, bool f32, hipStream_t stream) {
   if (total_tiles <= 0) return hipSuccess;
+  if (!f32) {
+    hipLaunchKernelGGL(gemm_wide_kernel, dim3(total_tiles), dim3(kWideThreads), 0, stream, a,
+                       total_tiles);
+    return hipGetLastError();
+  }
   if (f32)
     hipLaunchKernelGGL(gemm_nt_kernel<F32>, dim3(total_tiles), dim3(kThreads), 0, stream, a);
   else

@@ -12,7 +12,8 @@ namespace mls {
 constexpr int kMaxModels = 8;
 
 // Tile of the fused logits kernels: BM vocabulary rows x BN token columns.
-constexpr int kFusedBM = 128;
+constexpr int kFusedBM = 128;      // general core
+constexpr int kFusedWideBM = 256;  // wide bf16 core (all widths multiples of 64)
 constexpr int kFusedBN = 128;
 // Tile of the backward GEMMs.
 constexpr int kGemmBM = 128;
@@ -38,6 +39,7 @@ struct FusedArgs {
   int64_t ignore_index;
   float tau;
   float inv_tau;
+  int32_t wide;  // 1: wide bf16 core (BM = kFusedWideBM)
   int32_t n_tt;  // token tiles
   int32_t n_vt;  // vocabulary tiles in this launch
   // forward
@@ -119,8 +121,12 @@ struct RowArgs {
 };
 
 // Launchers (each enqueues on `stream` and returns the launch status).
+int fused_tile_rows(bool wide);
 hipError_t launch_fused_fwd(const FusedArgs& a, bool f32, hipStream_t stream);
 hipError_t launch_fused_bwd(const FusedArgs& a, bool f32, hipStream_t stream);
+// Output tile of the backward GEMMs for the given input dtype.
+int gemm_tile_rows(bool f32);
+int gemm_tile_cols(bool f32);
 hipError_t launch_gemm_nt(const GemmArgs& a, int total_tiles, bool f32, hipStream_t stream);
 hipError_t launch_transpose(const TransposeArgs& a, int64_t max_out_rows, int64_t max_cols,
                             bool f32, hipStream_t stream);
