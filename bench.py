@@ -39,6 +39,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample rows (0 = auto)")
     ap.add_argument("--vocab-chunk", type=int, default=0)
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="after timing, run one plain device copy of this many MiB (a known-size "
+                         "kernel to calibrate HBM byte counters)")
     return ap.parse_args()
 
 
@@ -160,11 +163,12 @@ def main():
                           "avg_launch_ms": tot / launches}
         log(f"  {kname:14s} {launches / args.steps:5.1f} launches/step "
             f"{tot / args.steps:8.3f} ms/step  avg {tot / launches:8.4f} ms")
-    # each of the four MFMA kernels performs one 2*T*V*sum(d) contraction per step
-    dense = {"fused_fwd", "fused_bwd", "gemm_grad_W", "gemm_grad_h"}
+    # dense work per step of each MFMA kernel: the forward and the recompute each
+    # contract 2*T*V*sum(d); the gradient GEMM launch holds both head products
+    one = 2.0 * wl.T * wl.V * sum(wl.dims)
+    dense = {"fused_fwd": one, "fused_bwd": one, "gemm_grads": 2.0 * one}
     dom = max((k for k in kernels if k in dense), key=lambda k: kernels[k]["ms_per_step"])
-    per_step = 2.0 * wl.T * wl.V * sum(wl.dims)
-    per_launch = per_step / kernels[dom]["launches_per_step"]
+    per_launch = dense[dom] / kernels[dom]["launches_per_step"]
     achieved = per_launch / (kernels[dom]["avg_launch_ms"] / 1e3)
     roofline = {
         "bound": "mfma",
@@ -175,6 +179,15 @@ def main():
         "frac": achieved / peak,
         "traffic": None,
     }
+
+    if args.copy_mib > 0:
+        src = torch.ones(args.copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy of {args.copy_mib} MiB done")
+        del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -82,7 +82,7 @@ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-constexpr int64_t kSlabTargetBytes = 256ll << 20;  // G and G^T slabs together
+constexpr int64_t kSlabTargetBytes = 512ll << 20;  // G and G^T slabs together
 
 struct Plan {
   int M = 0;
@@ -211,6 +211,7 @@ void fill_common(const mls_problem* p, const Plan& pl, FusedArgs& a) {
   a.tau = p->tau;
   a.inv_tau = 1.0f / p->tau;
   a.wide = pl.wide ? 1 : 0;
+  a.group_v = 8;
   a.n_tt = pl.n_tt;
   a.T_pad = pl.T_pad;
   a.Vc = pl.Vc;
@@ -458,42 +459,14 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
     }
     if (e != hipSuccess) return hip_fail(e, "fused backward launch");
 
-    // grad_W_i[chunk] = G_i^T h_i
-    GemmArgs gw;
-    memset(&gw, 0, sizeof(gw));
-    gw.K = pl.T_pad;
+    // grad_h_i (+)= G_i W_i[chunk] and grad_W_i[chunk] = G_i^T h_i in one grouped
+    // launch (the longer grad_h tiles first)
+    GemmArgs ga;
+    memset(&ga, 0, sizeof(ga));
     int tiles = 0;
     for (int i = 0; i < pl.M; ++i) {
-      if (!grad_W[i]) continue;
-      GemmGroup& g = gw.g[gw.ngroups++];
-      g.A = static_cast<const char*>(a.slabT) + (size_t)i * slab_stride;
-      g.B = hT + (size_t)doff[i] * pl.T_pad * pl.es;
-      g.C = grad_W[i] + v0 * p->d[i];
-      g.lda = pl.T_pad;
-      g.ldb = pl.T_pad;
-      g.ldc = p->d[i];
-      g.rows = vrows;
-      g.cols = p->d[i];
-      g.tiles_m = (int)((vrows + tbm - 1) / tbm);
-      g.tiles_n = (int)((p->d[i] + tbn - 1) / tbn);
-      g.tile_begin = tiles;
-      g.accumulate = (p->flags & MLS_ACCUMULATE_GRAD_W) ? 1 : 0;
-      tiles += g.tiles_m * g.tiles_n;
-    }
-    {
-      ProfScope ps("gemm_grad_W", s);
-      e = launch_gemm_nt(gw, tiles, pl.f32, s);
-    }
-    if (e != hipSuccess) return hip_fail(e, "grad_W launch");
-
-    // grad_h_i (+)= G_i W_i[chunk]
-    GemmArgs gh;
-    memset(&gh, 0, sizeof(gh));
-    gh.K = pl.Vc;
-    tiles = 0;
-    for (int i = 0; i < pl.M; ++i) {
       if (!grad_h[i]) continue;
-      GemmGroup& g = gh.g[gh.ngroups++];
+      GemmGroup& g = ga.g[ga.ngroups++];
       g.A = static_cast<const char*>(a.slab) + (size_t)i * slab_stride;
       g.B = WT + (size_t)doff[i] * pl.Vc * pl.es;
       g.C = grad_h[i];
@@ -502,17 +475,50 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
       g.ldc = p->d[i];
       g.rows = pl.T;
       g.cols = p->d[i];
+      g.K = pl.Vc;
       g.tiles_m = (int)((pl.T + tbm - 1) / tbm);
       g.tiles_n = (int)((p->d[i] + tbn - 1) / tbn);
       g.tile_begin = tiles;
       g.accumulate = (c > 0 || (p->flags & MLS_ACCUMULATE_GRAD_H)) ? 1 : 0;
+      g.group_m = 8;
       tiles += g.tiles_m * g.tiles_n;
     }
-    {
-      ProfScope ps("gemm_grad_h", s);
-      e = launch_gemm_nt(gh, tiles, pl.f32, s);
+    const int grad_h_tiles = tiles;
+    for (int i = 0; i < pl.M; ++i) {
+      if (!grad_W[i]) continue;
+      GemmGroup& g = ga.g[ga.ngroups++];
+      g.A = static_cast<const char*>(a.slabT) + (size_t)i * slab_stride;
+      g.B = hT + (size_t)doff[i] * pl.T_pad * pl.es;
+      g.C = grad_W[i] + v0 * p->d[i];
+      g.lda = pl.T_pad;
+      g.ldb = pl.T_pad;
+      g.ldc = p->d[i];
+      g.rows = vrows;
+      g.cols = p->d[i];
+      g.K = pl.T_pad;
+      g.tiles_m = (int)((vrows + tbm - 1) / tbm);
+      g.tiles_n = (int)((p->d[i] + tbn - 1) / tbn);
+      g.tile_begin = tiles;
+      g.accumulate = (p->flags & MLS_ACCUMULATE_GRAD_W) ? 1 : 0;
+      g.group_m = 0;
+      tiles += g.tiles_m * g.tiles_n;
     }
-    if (e != hipSuccess) return hip_fail(e, "grad_h launch");
+    // spread both phases evenly over the XCDs when every XCD's share of the
+    // first phase fits in its block count
+    ga.phase_tiles = 0;
+    if (grad_h_tiles > 0 && grad_h_tiles < tiles) {
+      bool fits = true;
+      for (int x = 0; x < 8; ++x) {
+        const int q1 = grad_h_tiles / 8 + (x < grad_h_tiles % 8 ? 1 : 0);
+        if (q1 > (tiles - x + 7) / 8) fits = false;
+      }
+      if (fits) ga.phase_tiles = grad_h_tiles;
+    }
+    {
+      ProfScope ps("gemm_grads", s);
+      e = launch_gemm_nt(ga, tiles, pl.f32, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "gradient GEMM launch");
   }
   return MLS_OK;
 }

@@ -42,6 +42,39 @@ __device__ __forceinline__ int xcd_remap(int b, int nb) {
   return x * q + (x < r ? x : r) + b / 8;
 }
 
+// Like xcd_remap for a launch whose first n1 tiles cost more than the rest:
+// every XCD gets an even share of each phase, as one contiguous range per
+// phase. Requires every XCD's share of phase 1 to fit in its block count
+// (the host passes n1 = 0, i.e. plain xcd_remap, otherwise).
+__device__ __forceinline__ int xcd_remap_phased(int b, int nb, int n1) {
+  if (n1 <= 0 || n1 >= nb) return xcd_remap(b, nb);
+  const int x = b % 8;
+  const int i = b / 8;
+  const int q = n1 / 8;
+  const int r = n1 % 8;
+  const int q1 = q + (x < r ? 1 : 0);
+  if (i < q1) return x * q + (x < r ? x : r) + i;
+  int start2 = 0;
+  for (int y = 0; y < x; ++y) start2 += (nb - y + 7) / 8 - (q + (y < r ? 1 : 0));
+  return n1 + start2 + (i - q1);
+}
+
+// Logical tile index -> (vocabulary tile, token tile). Tiles are taken in
+// groups of `group_v` vocabulary tiles; inside a group the vocabulary tile
+// varies fastest, so the blocks resident on one XCD at a time cover a
+// rectangle of about group_v vocabulary tiles x (32 / group_v) token tiles
+// and both operand panels are re-read from L2 rather than from memory.
+__device__ __forceinline__ void tile_coords(int bl, int n_vt, int n_tt, int group_v, int& vt,
+                                            int& tt) {
+  const int per_group = group_v * n_tt;
+  const int g = bl / per_group;
+  const int first = g * group_v;
+  const int gsz = (n_vt - first) < group_v ? (n_vt - first) : group_v;
+  const int in = bl - g * per_group;
+  vt = first + in % gsz;
+  tt = in / gsz;
+}
+
 template <int BM, int BN, int WGM, int WGN, int STAGES>
 struct WideMma {
   static constexpr int kBM = BM;

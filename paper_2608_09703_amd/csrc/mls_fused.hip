@@ -30,7 +30,7 @@ namespace {
 // (widths multiples of 64).
 using GenMmaBf16 = TileMma<Bf16, kFusedBM, kFusedBN, 2, 2>;
 using GenMmaF32 = TileMma<F32, kFusedBM, kFusedBN, 2, 2>;
-using WideFused = WideMma<kFusedWideBM, kFusedBN, 2, 2, 2>;
+using WideFused = WideMma<kFusedWideBM, kFusedBN, 2, 2, 2>;  // 2 blocks per CU
 
 // Per-lane copy of the teacher's tile values (its softmax weights), laid out
 // like the accumulators. The bf16 paths keep them as packed bf16 pairs
@@ -78,8 +78,8 @@ __global__ __launch_bounds__(Mma::NT, MINB) void fused_fwd_kernel(FusedArgs a) {
   const int wn = wave / WGM;
   const int hi = lane >> 5;
   const int bl = xcd_remap(blockIdx.x, gridDim.x);
-  const int tt = bl % a.n_tt;
-  const int vt = bl / a.n_tt;
+  int vt, tt;
+  tile_coords(bl, a.n_vt, a.n_tt, a.group_v, vt, tt);
   const int64_t vbase = (int64_t)vt * BM;
   const int64_t tbase = (int64_t)tt * BN;
   const bool full = vbase + BM <= a.V;
@@ -216,8 +216,8 @@ __global__ __launch_bounds__(Mma::NT, 1) void fused_bwd_kernel(FusedArgs a) {
   const int wm = wave % WGM;
   const int wn = wave / WGM;
   const int bl = xcd_remap(blockIdx.x, gridDim.x);
-  const int tt = bl % a.n_tt;
-  const int vt = bl / a.n_tt;
+  int vt, tt;
+  tile_coords(bl, a.n_vt, a.n_tt, a.group_v, vt, tt);
   const int64_t vloc = (int64_t)vt * BM;  // row offset inside the chunk
   const int64_t vbase = a.v0 + vloc;      // absolute vocabulary row
   const int64_t tbase = (int64_t)tt * BN;
@@ -303,15 +303,19 @@ __global__ __launch_bounds__(Mma::NT, 1) void fused_bwd_kernel(FusedArgs a) {
 // rows by plain copies, vocabulary-major rows through transposing LDS reads
 // (ds_read_b64_tr_b16: within a 16-lane group, lane j addresses row k0 + j/4,
 // column n0 + 4 (j % 4); lane i receives column n0 + i of rows k0 .. k0 + 3).
-template <bool TAU1>
-__global__ __launch_bounds__(256, 1) void fused_bwd_wide_kernel(FusedArgs a) {
-  using Mma = WideFused;
-  constexpr int BM = Mma::kBM;  // 256 vocabulary rows
-  constexpr int BN = Mma::kBN;  // 128 tokens
+template <class Mma, bool TAU1, int MINB>
+__global__ __launch_bounds__(Mma::NT, MINB) void fused_bwd_wide_kernel(FusedArgs a) {
+  constexpr int BM = Mma::kBM;  // vocabulary rows
+  constexpr int BN = Mma::kBN;  // tokens
   constexpr int WGM = Mma::kWGM;
   constexpr int FM = Mma::FM;
   constexpr int FN = Mma::FN;
-  constexpr int kGRow = BM * 2;  // bytes per token row of the staged tile
+  constexpr int NT = Mma::NT;
+  constexpr int NWV = NT / 64;
+  constexpr int kGRow = BM * 2;     // bytes per token row of the staged tile
+  constexpr int kChunks = BM / 8;   // 16-byte chunks per token row
+  constexpr int kCMask = kChunks - 1;
+  static_assert((kChunks & kCMask) == 0 && kChunks <= 32, "row chunk count is a power of two");
   static_assert(BN * kGRow <= Mma::kSmemBytes, "staged tile fits in the stage memory");
   typedef short v4s_t __attribute__((ext_vector_type(4)));
   __shared__ __attribute__((aligned(16))) char smem[Mma::kSmemBytes];
@@ -322,8 +326,8 @@ __global__ __launch_bounds__(256, 1) void fused_bwd_wide_kernel(FusedArgs a) {
   const int wm = wave % WGM;
   const int wn = wave / WGM;
   const int bl = xcd_remap(blockIdx.x, gridDim.x);
-  const int tt = bl % a.n_tt;
-  const int vt = bl / a.n_tt;
+  int vt, tt;
+  tile_coords(bl, a.n_vt, a.n_tt, a.group_v, vt, tt);
   const int64_t vloc = (int64_t)vt * BM;
   const int64_t vbase = a.v0 + vloc;
   const int64_t tbase = (int64_t)tt * BN;
@@ -394,38 +398,38 @@ __global__ __launch_bounds__(256, 1) void fused_bwd_wide_kernel(FusedArgs a) {
           uint2 w;
           w.x = (uint32_t)to_storage<Bf16>(g[0]) | ((uint32_t)to_storage<Bf16>(g[1]) << 16);
           w.y = (uint32_t)to_storage<Bf16>(g[2]) | ((uint32_t)to_storage<Bf16>(g[3]) << 16);
-          const int off = trow * kGRow + ((((v0 >> 3) ^ (trow & 31))) << 4) + ((v0 >> 2) & 1) * 8;
+          const int off = trow * kGRow + ((((v0 >> 3) ^ (trow & kCMask))) << 4) + ((v0 >> 2) & 1) * 8;
           *reinterpret_cast<uint2*>(smem + off) = w;
           __builtin_amdgcn_sched_barrier(0);  // bound live ranges: one 4-row group at a time
         }
     }
     block_barrier();
 
-    // 2. token-major slab: 128 rows x 32 chunks of 16 bytes
+    // 2. token-major slab: BN rows x kChunks chunks of 16 bytes
     uint16_t* slab = static_cast<uint16_t*>(a.slab) + (int64_t)i * a.T_pad * a.Vc;
     uint16_t* slabT = static_cast<uint16_t*>(a.slabT) + (int64_t)i * a.T_pad * a.Vc;
 #pragma unroll 4
-    for (int j = 0; j < BN * 32 / 256; ++j) {
-      const int idx = tid + 256 * j;
-      const int t = idx >> 5;
-      const int c = idx & 31;
-      const uint4 v = *reinterpret_cast<const uint4*>(smem + t * kGRow + ((c ^ (t & 31)) << 4));
+    for (int j = 0; j < BN * kChunks / NT; ++j) {
+      const int idx = tid + NT * j;
+      const int t = idx / kChunks;
+      const int c = idx & kCMask;
+      const uint4 v = *reinterpret_cast<const uint4*>(smem + t * kGRow + ((c ^ (t & kCMask)) << 4));
       *reinterpret_cast<uint4*>(slab + (tbase + t) * a.Vc + vloc + c * 8) = v;
     }
-    // 3. vocabulary-major slab: 256 rows x 16 chunks of 8 tokens, via transposing reads
+    // 3. vocabulary-major slab: BM rows x BN/8 chunks of 8 tokens, via transposing reads
     {
       const int grp = lane >> 4;
       const int j16 = lane & 15;
 #pragma unroll 2
-      for (int it = 0; it < (BM / 16) * (BN / 8) / 16; ++it) {
-        const int task = (it * 4 + wave) * 4 + grp;
+      for (int it = 0; it < (BM / 16) * (BN / 8) / (4 * NWV); ++it) {
+        const int task = (it * NWV + wave) * 4 + grp;
         const int vb = (task % (BM / 16)) * 16;
         const int k0 = (task / (BM / 16)) * 8;
         const int vv = vb + 4 * (j16 & 3);
         const int ta = k0 + (j16 >> 2);
         const int tb = ta + 4;
-        const int oa = ta * kGRow + (((vv >> 3) ^ (ta & 31)) << 4) + (vv & 7) * 2;
-        const int ob = tb * kGRow + (((vv >> 3) ^ (tb & 31)) << 4) + (vv & 7) * 2;
+        const int oa = ta * kGRow + (((vv >> 3) ^ (ta & kCMask)) << 4) + (vv & 7) * 2;
+        const int ob = tb * kGRow + (((vv >> 3) ^ (tb & kCMask)) << 4) + (vv & 7) * 2;
         const v4s_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
             (__attribute__((address_space(3))) v4s_t*)((__attribute__((address_space(3))) char*)smem + oa));
         const v4s_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -465,9 +469,16 @@ hipError_t launch_fused_fwd(const FusedArgs& a, bool f32, hipStream_t stream) {
   if (f32)
     return tau1 ? launch_fwd_t<GenMmaF32, F32, true>(a, stream)
                 : launch_fwd_t<GenMmaF32, F32, false>(a, stream);
-  if (a.wide)
-    return tau1 ? launch_fwd_t<WideFused, Bf16, true>(a, stream)
-                : launch_fwd_t<WideFused, Bf16, false>(a, stream);
+  if (a.wide) {
+    dim3 grid((unsigned)a.n_tt * (unsigned)a.n_vt);
+    if (tau1)
+      hipLaunchKernelGGL((fused_fwd_kernel<WideFused, Bf16, true, 2>), grid, dim3(WideFused::NT), 0,
+                         stream, a);
+    else
+      hipLaunchKernelGGL((fused_fwd_kernel<WideFused, Bf16, false, 2>), grid, dim3(WideFused::NT), 0,
+                         stream, a);
+    return hipGetLastError();
+  }
   return tau1 ? launch_fwd_t<GenMmaBf16, Bf16, true>(a, stream)
               : launch_fwd_t<GenMmaBf16, Bf16, false>(a, stream);
 }
@@ -480,9 +491,11 @@ hipError_t launch_fused_bwd(const FusedArgs& a, bool f32, hipStream_t stream) {
   if (a.wide) {
     dim3 grid((unsigned)a.n_tt * (unsigned)a.n_vt);
     if (tau1)
-      hipLaunchKernelGGL(fused_bwd_wide_kernel<true>, grid, dim3(WideFused::NT), 0, stream, a);
+      hipLaunchKernelGGL((fused_bwd_wide_kernel<WideFused, true, 2>), grid, dim3(WideFused::NT), 0,
+                         stream, a);
     else
-      hipLaunchKernelGGL(fused_bwd_wide_kernel<false>, grid, dim3(WideFused::NT), 0, stream, a);
+      hipLaunchKernelGGL((fused_bwd_wide_kernel<WideFused, false, 2>), grid, dim3(WideFused::NT), 0,
+                         stream, a);
     return hipGetLastError();
   }
   return tau1 ? launch_bwd_t<GenMmaBf16, Bf16, true>(a, stream)

@@ -1,6 +1,6 @@
 // The two backward products of the LM head (the head is linear, paper
-// section 2, "Modeling"), per vocabulary chunk and for every sub-model in one
-// grouped launch:
+// section 2, "Modeling"), per vocabulary chunk, both products for every
+// sub-model in one grouped launch:
 //   grad_W_i[chunk] = G_i^T h_i       A = G_i^T slab [Vc, T_pad], B = h_i^T [d_i, T_pad]
 //   grad_h_i       += G_i W_i[chunk]  A = G_i slab   [T_pad, Vc], B = W_i[chunk]^T [d_i, Vc]
 // Both are NT tile products on the shared MFMA main loop; the transposed
@@ -38,7 +38,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_nt_kernel(GemmArgs a) {
 
   Mma mma;
   mma.run(static_cast<const char*>(g.A), g.lda * E::kBytes, m0, g.rows,
-          static_cast<const char*>(g.B), g.ldb * E::kBytes, n0, g.cols, a.K * E::kBytes, smem,
+          static_cast<const char*>(g.B), g.ldb * E::kBytes, n0, g.cols, g.K * E::kBytes, smem,
           tid);
 
 #pragma unroll
@@ -74,20 +74,25 @@ __global__ __launch_bounds__(kWideThreads, 2) void gemm_wide_kernel(GemmArgs a, 
   const int wave = tid >> 6;
   const int wm = wave % 2;
   const int wn = wave / 2;
-  const int b = xcd_remap(blockIdx.x, nb);
+  const int b = xcd_remap_phased(blockIdx.x, nb, a.phase_tiles);
   int gi = 0;
   for (int k = 1; k < a.ngroups; ++k)
     if (b >= a.g[k].tile_begin) gi = k;
   const GemmGroup& g = a.g[gi];
   const int local = b - g.tile_begin;
-  const int tn = local % g.tiles_n;
-  const int tm = local / g.tiles_n;
+  int tm, tn;
+  if (g.group_m > 0) {
+    tile_coords(local, g.tiles_m, g.tiles_n, g.group_m, tm, tn);
+  } else {
+    tn = local % g.tiles_n;
+    tm = local / g.tiles_n;
+  }
   const int64_t m0 = (int64_t)tm * kWideBM;
   const int64_t n0 = (int64_t)tn * kWideBN;
 
   Mma mma;
   mma.run(static_cast<const char*>(g.A), g.lda * 2, m0, g.rows, static_cast<const char*>(g.B),
-          g.ldb * 2, n0, g.cols, a.K * 2, smem, tid);
+          g.ldb * 2, n0, g.cols, g.K * 2, smem, tid);
 
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm)

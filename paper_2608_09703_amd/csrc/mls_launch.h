@@ -13,7 +13,7 @@ constexpr int kMaxModels = 8;
 
 // Tile of the fused logits kernels: BM vocabulary rows x BN token columns.
 constexpr int kFusedBM = 128;      // general core
-constexpr int kFusedWideBM = 256;  // wide bf16 core (all widths multiples of 64)
+constexpr int kFusedWideBM = 128;  // wide bf16 core (all widths multiples of 64)
 constexpr int kFusedBN = 128;
 // Tile of the backward GEMMs.
 constexpr int kGemmBM = 128;
@@ -40,6 +40,7 @@ struct FusedArgs {
   float tau;
   float inv_tau;
   int32_t wide;  // 1: wide bf16 core (BM = kFusedWideBM)
+  int32_t group_v;  // vocabulary tiles per ordering group (see tile_coords), >= 1
   int32_t n_tt;  // token tiles
   int32_t n_vt;  // vocabulary tiles in this launch
   // forward
@@ -69,16 +70,22 @@ struct GemmGroup {
   int64_t ldc;
   int64_t rows;  // m extent
   int64_t cols;  // n extent
+  int64_t K;     // contraction length in elements (a multiple of the LDS row)
   int32_t tiles_m;
   int32_t tiles_n;
   int32_t tile_begin;
   int32_t accumulate;
+  int32_t group_m;  // tile order: 0 = n fastest; g > 0 = groups of g row tiles, rows fastest
 };
+
+constexpr int kMaxGemmGroups = 2 * kMaxModels;
 
 struct GemmArgs {
   int32_t ngroups;
-  int64_t K;  // contraction length in elements (a multiple of the LDS row)
-  GemmGroup g[kMaxModels];
+  // Tiles [0, phase_tiles) and [phase_tiles, total) have different costs (K);
+  // each phase is spread evenly over the XCDs. 0 = one phase.
+  int32_t phase_tiles;
+  GemmGroup g[kMaxGemmGroups];
 };
 
 // dst[c][r] = src[(r0 + r) * ld_src + c] for r0 + r < src_rows, else 0;
