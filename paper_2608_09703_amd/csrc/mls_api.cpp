@@ -82,7 +82,7 @@ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-constexpr int64_t kSlabTargetBytes = 512ll << 20;  // G and G^T slabs together
+constexpr int64_t kSlabTargetBytes = 512ll << 20;  // logit-gradient slab(s) per chunk
 
 struct Plan {
   int M = 0;
@@ -156,7 +156,8 @@ void make_plan(const mls_problem* p, Plan& pl) {
   if (p->vocab_chunk > 0) {
     vc = round_up(p->vocab_chunk, 256);
   } else {
-    vc = kSlabTargetBytes / (2ll * pl.M * pl.T_pad * pl.es);
+    // the wide path keeps one slab layout, the general path two
+    vc = kSlabTargetBytes / ((pl.wide ? 1ll : 2ll) * pl.M * pl.T_pad * pl.es);
     vc = vc / 256 * 256;
   }
   pl.Vc = std::max<int64_t>(256, std::min(vc, vmax));
@@ -173,12 +174,14 @@ void make_plan(const mls_problem* p, Plan& pl) {
   const size_t slab = (size_t)pl.M * pl.T_pad * pl.Vc * pl.es;
   pl.off_slab = off;
   off = align256(off + slab);
-  pl.off_slabT = off;
-  off = align256(off + slab);
-  pl.off_hT = off;
-  off = align256(off + (size_t)pl.sumd * pl.T_pad * pl.es);
-  pl.off_WT = off;
-  off = align256(off + (size_t)pl.sumd * pl.Vc * pl.es);
+  if (!pl.wide) {  // general path: G^T slab and transposed operands as well
+    pl.off_slabT = off;
+    off = align256(off + slab);
+    pl.off_hT = off;
+    off = align256(off + (size_t)pl.sumd * pl.T_pad * pl.es);
+    pl.off_WT = off;
+    off = align256(off + (size_t)pl.sumd * pl.Vc * pl.es);
+  }
   pl.bwd_bytes = off;
   pl.ws_bytes = std::max(pl.fwd_bytes, pl.bwd_bytes);
 
@@ -385,7 +388,7 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
   a.g_kl = g_kl;
   host_coeffs(pl.M, pl.s, p->alpha, p->tau, MLS_MODE_PAPER, nullptr, a.host_gce, a.host_gkl);
   a.slab = ws + pl.off_slab;
-  a.slabT = ws + pl.off_slabT;
+  a.slabT = pl.wide ? nullptr : ws + pl.off_slabT;
   char* hT = ws + pl.off_hT;
   char* WT = ws + pl.off_WT;
 
@@ -396,12 +399,12 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
     acc += p->d[i];
   }
   const size_t slab_stride = (size_t)pl.T_pad * pl.Vc * pl.es;
-  const int tbm = gemm_tile_rows(pl.f32);
-  const int tbn = gemm_tile_cols(pl.f32);
+  const int tbm = gemm_tile_rows(pl.wide);
+  const int tbn = gemm_tile_cols(pl.wide);
   hipError_t e;
 
-  // h_i^T [d_i, T_pad] for the grad_W products
-  {
+  // general path: h_i^T [d_i, T_pad] for the grad_W products
+  if (!pl.wide) {
     TransposeArgs ta;
     memset(&ta, 0, sizeof(ta));
     int64_t maxc = 0;
@@ -429,7 +432,8 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
     const int64_t v0 = (int64_t)c * pl.Vc;
     const int64_t vrows = std::min(pl.Vc, pl.V - v0);
 
-    // W_i[chunk]^T [d_i, Vc] for the grad_h products
+    // general path: W_i[chunk]^T [d_i, Vc] for the grad_h products
+    if (!pl.wide) {
     TransposeArgs ta;
     memset(&ta, 0, sizeof(ta));
     int64_t maxc = 0;
@@ -451,6 +455,7 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
       e = launch_transpose(ta, pl.Vc, maxc, pl.f32, s);
     }
     if (e != hipSuccess) return hip_fail(e, "transpose launch");
+    }
 
     a.v0 = v0;
     {
@@ -460,7 +465,9 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
     if (e != hipSuccess) return hip_fail(e, "fused backward launch");
 
     // grad_h_i (+)= G_i W_i[chunk] and grad_W_i[chunk] = G_i^T h_i in one grouped
-    // launch (the longer grad_h tiles first)
+    // launch (the longer grad_h tiles first). The wide path reads the slab, the
+    // head chunk and h in their stored layouts; the general path reads G^T and
+    // the transposed operands.
     GemmArgs ga;
     memset(&ga, 0, sizeof(ga));
     int tiles = 0;
@@ -468,14 +475,22 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
       if (!grad_h[i]) continue;
       GemmGroup& g = ga.g[ga.ngroups++];
       g.A = static_cast<const char*>(a.slab) + (size_t)i * slab_stride;
-      g.B = WT + (size_t)doff[i] * pl.Vc * pl.es;
-      g.C = grad_h[i];
       g.lda = pl.Vc;
-      g.ldb = pl.Vc;
-      g.ldc = p->d[i];
       g.rows = pl.T;
-      g.cols = p->d[i];
+      if (pl.wide) {
+        g.B = static_cast<const char*>(p->W[i]) + (size_t)v0 * p->d[i] * pl.es;  // [v][d]
+        g.ldb = p->d[i];
+        g.cols = vrows;
+      } else {
+        g.B = WT + (size_t)doff[i] * pl.Vc * pl.es;
+        g.ldb = pl.Vc;
+        g.cols = p->d[i];
+      }
+      g.C = grad_h[i];
+      g.ldc = p->d[i];
+      g.ldc_rows = pl.T;
       g.K = pl.Vc;
+      g.kind = 0;
       g.tiles_m = (int)((pl.T + tbm - 1) / tbm);
       g.tiles_n = (int)((p->d[i] + tbn - 1) / tbn);
       g.tile_begin = tiles;
@@ -487,15 +502,26 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
     for (int i = 0; i < pl.M; ++i) {
       if (!grad_W[i]) continue;
       GemmGroup& g = ga.g[ga.ngroups++];
-      g.A = static_cast<const char*>(a.slabT) + (size_t)i * slab_stride;
-      g.B = hT + (size_t)doff[i] * pl.T_pad * pl.es;
+      if (pl.wide) {
+        g.A = static_cast<const char*>(a.slab) + (size_t)i * slab_stride;  // [t][v]
+        g.lda = pl.Vc;
+        g.rows = pl.T_pad;
+        g.B = p->h[i];  // [t][d]
+        g.ldb = p->d[i];
+        g.cols = pl.T;
+      } else {
+        g.A = static_cast<const char*>(a.slabT) + (size_t)i * slab_stride;
+        g.lda = pl.T_pad;
+        g.rows = vrows;
+        g.B = hT + (size_t)doff[i] * pl.T_pad * pl.es;
+        g.ldb = pl.T_pad;
+        g.cols = p->d[i];
+      }
       g.C = grad_W[i] + v0 * p->d[i];
-      g.lda = pl.T_pad;
-      g.ldb = pl.T_pad;
       g.ldc = p->d[i];
-      g.rows = vrows;
-      g.cols = p->d[i];
+      g.ldc_rows = vrows;
       g.K = pl.T_pad;
+      g.kind = 1;
       g.tiles_m = (int)((vrows + tbm - 1) / tbm);
       g.tiles_n = (int)((p->d[i] + tbn - 1) / tbn);
       g.tile_begin = tiles;
@@ -516,7 +542,7 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
     }
     {
       ProfScope ps("gemm_grads", s);
-      e = launch_gemm_nt(ga, tiles, pl.f32, s);
+      e = pl.wide ? launch_gemm_wide(ga, tiles, s) : launch_gemm_nt(ga, tiles, pl.f32, s);
     }
     if (e != hipSuccess) return hip_fail(e, "gradient GEMM launch");
   }

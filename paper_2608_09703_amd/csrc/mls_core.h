@@ -10,10 +10,11 @@
 //    descriptor covers the block's operand panel, so per-lane offsets are
 //    32-bit, fixed for the whole K loop (the K position is a scalar offset),
 //    and rows past the end of the operand read as zero;
-//  - STAGES K-tiles of 64 bf16 are in flight; a K-tile is consumed after an
+//  - STAGES K-tiles of RB bytes (64 or 32 bf16) are in flight; a K-tile is consumed after an
 //    explicit vmcnt wait and a plain s_barrier (no memory fence, so younger
 //    loads stay in flight across the barrier);
-//  - K must be a multiple of 64 and the operand row stride at least K; a
+//  - K must be a multiple of 64 (RB = 128) or 32 (RB = 64) and the operand
+//    row stride at least K; a
 //    panel must be below 4 GiB.
 #pragma once
 
@@ -75,7 +76,44 @@ __device__ __forceinline__ void tile_coords(int bl, int n_vt, int n_tt, int grou
   tt = in / gsz;
 }
 
-template <int BM, int BN, int WGM, int WGN, int STAGES>
+// LDS placement for tiles whose rows hold RB bytes of K (RB = 128 or 64):
+// 16-byte chunk c of row `row` lives at chunk position c ^ swz(row). For
+// 128-byte rows, rows r..r+7 and r, r+8 differ; for 64-byte rows (4 chunks)
+// the XOR is ((row >> 1) & 3) ^ (3 * bit3(row)), which is a bijection over 16
+// aligned rows sharing row % 4 and over 8 aligned rows sharing row % 2, so
+// fragment reads are conflict-free for 8- and 16-lane read phases alike.
+template <int RB>
+__device__ __forceinline__ int swz_chunk(int row, int c) {
+  if (RB == 128) return c ^ (row & 7) ^ ((row >> 3) & 1);
+  return c ^ ((row >> 1) & 3) ^ (((row >> 3) & 1) * 3);
+}
+
+template <int RB>
+__device__ __forceinline__ uint4 lds_read16_rb(const char* base, int row, int c) {
+  return *reinterpret_cast<const uint4*>(base + row * RB + (swz_chunk<RB>(row, c) << 4));
+}
+
+// Operand layouts: KC = row-major [m][k] (K contiguous, the MFMA's natural
+// operand order); MC = row-major [k][m] (M contiguous). An MC tile is staged
+// in LDS as stored (K-tile rows of BM*2 bytes) and its fragments are read with
+// ds_read_b64_tr_b16, which hands lane i of each 16-lane group column m0+i of
+// four consecutive rows. Two such reads give the 8 consecutive K values of
+// one MFMA operand. Chunks of a staged row are XOR-swizzled with 2*(k % 4)
+// so the four rows one group reads fall in distinct banks.
+enum { kLayoutKC = 0, kLayoutMC = 1 };
+
+typedef short v4s_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ int mc_chunk(int krow, int c) { return c ^ ((krow & 3) << 1); }
+
+__device__ __forceinline__ uint2 lds_read_tr8(const char* p) {
+  const v4s_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4s_t*)((__attribute__((address_space(3))) char*)p));
+  return __builtin_bit_cast(uint2, v);
+}
+
+template <int BM, int BN, int WGM, int WGN, int STAGES, int RB = 128, int ALAY = kLayoutKC,
+          int BLAY = kLayoutKC>
 struct WideMma {
   static constexpr int kBM = BM;
   static constexpr int kBN = BN;
@@ -87,12 +125,16 @@ struct WideMma {
   static constexpr int WTN = BN / WGN;
   static constexpr int FM = WTM / 32;
   static constexpr int FN = WTN / 32;
-  static constexpr int kStageBytes = (BM + BN) * kRowBytes;
+  static constexpr int CPR = RB / 16;     // 16-byte chunks per LDS row (KC layout)
+  static constexpr int KSTEPS = RB / 32;  // MFMA K-steps (16 bf16) per K-tile
+  static constexpr int BK = RB / 2;       // K values per K-tile
+  static constexpr int kStageBytes = (BM + BN) * RB;
   static constexpr int kSmemBytes = STAGES * kStageBytes;
-  static constexpr int LA = BM * 8 / NT;  // load instructions per thread per K-tile, A
-  static constexpr int LB = BN * 8 / NT;
+  static constexpr int LA = BM * CPR / NT;  // load instructions per thread per K-tile, A
+  static constexpr int LB = BN * CPR / NT;
   static constexpr int kLoadsPerTile = LA + LB;
-  static_assert(BM * 8 % NT == 0 && BN * 8 % NT == 0, "tile must split evenly over the waves");
+  static_assert(RB == 128 || RB == 64, "LDS rows of 64 or 128 bytes");
+  static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile must split evenly over the waves");
   static_assert(STAGES >= 2 && STAGES <= 4, "2..4 stages");
   static_assert(kLoadsPerTile * (STAGES - 1) < 64, "vmcnt range");
 
@@ -115,10 +157,36 @@ struct WideMma {
 #pragma unroll
     for (int j = 0; j < L; ++j) {
       const int slot = (j * NW + wave) * 64 + lane;
-      const int row = slot >> 3;
-      const int c = (slot & 7) ^ (row & 7) ^ ((row >> 3) & 1);
+      const int row = slot / CPR;
+      const int c = swz_chunk<RB>(row, slot % CPR);  // the XOR is an involution
       off[j] = (uint32_t)(row * ld_bytes) + (uint32_t)(c << 4);
     }
+  }
+
+  // MC operand: per-lane offsets of its chunks inside a K-tile of BK rows of
+  // ROWS*2 bytes (relative to the tile's first row and the block's column m0).
+  template <int ROWS, int L>
+  __device__ __forceinline__ static void panel_offsets_mc(int64_t ld_bytes, int wave, int lane,
+                                                          uint32_t* off) {
+    constexpr int CPM = ROWS / 8;  // chunks per staged row
+#pragma unroll
+    for (int j = 0; j < L; ++j) {
+      const int slot = (j * NW + wave) * 64 + lane;
+      const int krow = slot / CPM;
+      const int c = mc_chunk(krow, slot % CPM);
+      off[j] = (uint32_t)(krow * ld_bytes) + (uint32_t)(c << 4);
+    }
+  }
+
+  // MC operand panel: columns from m0 on, over the `nrows` stored rows (the
+  // K extent that exists in memory); reads past the end return 0, so K-tiles
+  // beyond nrows contribute nothing.
+  __device__ __forceinline__ static __amdgpu_buffer_rsrc_t panel_rsrc_mc(const char* base,
+                                                                         int64_t ld_bytes,
+                                                                         int64_t m0, int64_t nrows) {
+    const int64_t bytes = nrows * ld_bytes - m0 * 2;
+    return __builtin_amdgcn_make_buffer_rsrc((void*)(base + m0 * 2), (short)0,
+                                             (int)(bytes > 0 ? bytes : 0), 0x00020000);
   }
 
   __device__ __forceinline__ static __amdgpu_buffer_rsrc_t panel_rsrc(const char* base,
@@ -132,48 +200,72 @@ struct WideMma {
                                              (int)(avail * ld_bytes), 0x00020000);
   }
 
-  // Enqueue the direct loads of one operand tile (the panel's 128 bytes at kb0).
+  // Enqueue the direct loads of one operand tile. `vofs` is added to every
+  // lane's offset (it takes part in the descriptor's range check); `sofs` is
+  // the scalar offset (not range-checked, so only used where every lane's
+  // address stays inside its row: the K position of a KC operand).
   template <int L>
   __device__ __forceinline__ static void issue_operand(__amdgpu_buffer_rsrc_t rsrc,
-                                                       const uint32_t* off, int kb0, char* lds,
-                                                       int wave) {
+                                                       const uint32_t* off, uint32_t vofs,
+                                                       int sofs, char* lds, int wave) {
 #pragma unroll
     for (int j = 0; j < L; ++j) {
       char* dst = lds + (j * NW + wave) * 64 * 16;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t*)dst, 16, off[j], kb0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t*)dst, 16, off[j] + vofs, sofs, 0,
+                                               0);
     }
   }
 
-  // Fragment reads of sub-step kk+1 are interleaved with the MFMAs of
-  // sub-step kk (two register sets), so LDS latency hides behind the MFMA
-  // chain while at most FM+FN reads are outstanding.
-  __device__ __forceinline__ void load_frags(const char* pa, const char* pb, int kk, int lane,
-                                             uint4* a, uint4* b) {
+  // One MFMA operand fragment of an MC tile: row block `r0` (32 rows), K-step kk.
+  template <int ROWS>
+  __device__ __forceinline__ static uint4 mc_frag(const char* base, int r0, int kk, int lane) {
+    constexpr int RBYTES = ROWS * 2;
+    const int g = lane >> 4;
+    const int j = lane & 15;
+    const int m = r0 + (g & 1) * 16 + 4 * (j & 3);
+    const int k = kk * 16 + (g >> 1) * 8 + (j >> 2);
+    const int c = m >> 3;
+    const int in = (m & 7) * 2;
+    const uint2 lo = lds_read_tr8(base + k * RBYTES + (mc_chunk(k, c) << 4) + in);
+    const uint2 hi = lds_read_tr8(base + (k + 4) * RBYTES + (mc_chunk(k + 4, c) << 4) + in);
+    return make_uint4(lo.x, lo.y, hi.x, hi.y);
+  }
+
+  __device__ __forceinline__ void load_frags(const char* sA, const char* sB, int kk, int lane,
+                                             int wm, int wn, uint4* a, uint4* b) {
     const int c = 2 * kk + (lane >> 5);
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm) a[fm] = lds_read16(pa, fm * 32 + (lane & 31), c);
+    for (int fm = 0; fm < FM; ++fm) {
+      if (ALAY == kLayoutKC)
+        a[fm] = lds_read16_rb<RB>(sA + wm * WTM * RB, fm * 32 + (lane & 31), c);
+      else
+        a[fm] = mc_frag<BM>(sA, wm * WTM + fm * 32, kk, lane);
+    }
 #pragma unroll
-    for (int fn = 0; fn < FN; ++fn) b[fn] = lds_read16(pb, fn * 32 + (lane & 31), c);
+    for (int fn = 0; fn < FN; ++fn) {
+      if (BLAY == kLayoutKC)
+        b[fn] = lds_read16_rb<RB>(sB + wn * WTN * RB, fn * 32 + (lane & 31), c);
+      else
+        b[fn] = mc_frag<BN>(sB, wn * WTN + fn * 32, kk, lane);
+    }
   }
 
   __device__ __forceinline__ void compute_stage(const char* sA, const char* sB, int lane, int wm,
                                                 int wn) {
     constexpr int kMfma = FM * FN;
-    constexpr int kReads = FM + FN;
+    constexpr int kReads = (FM + FN) * ((ALAY == kLayoutMC || BLAY == kLayoutMC) ? 2 : 1);
     constexpr int kPer = kMfma / kReads > 0 ? kMfma / kReads : 1;  // MFMAs per read
-    const char* pa = sA + wm * WTM * kRowBytes;
-    const char* pb = sB + wn * WTN * kRowBytes;
     uint4 a[2][FM], b[2][FN];
-    load_frags(pa, pb, 0, lane, a[0], b[0]);
+    load_frags(sA, sB, 0, lane, wm, wn, a[0], b[0]);
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
+    for (int kk = 0; kk < KSTEPS; ++kk) {
       __builtin_amdgcn_sched_barrier(0);
-      if (kk < 3) load_frags(pa, pb, kk + 1, lane, a[(kk + 1) & 1], b[(kk + 1) & 1]);
+      if (kk < KSTEPS - 1) load_frags(sA, sB, kk + 1, lane, wm, wn, a[(kk + 1) & 1], b[(kk + 1) & 1]);
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
         for (int fn = 0; fn < FN; ++fn) mma_step<Bf16>(acc[fm][fn], a[kk & 1][fm], b[kk & 1][fn]);
-      if (kk < 3) {
+      if (kk < KSTEPS - 1) {
 #pragma unroll
         for (int q = 0; q < kReads; ++q) {
           __builtin_amdgcn_sched_group_barrier(0x008, kPer, 0);  // MFMA
@@ -185,6 +277,9 @@ struct WideMma {
   }
 
   // acc = A[a_row0 : +BM, :K] * B[b_row0 : +BN, :K]^T with K = kbytes / 2.
+  // a_rows / b_rows: rows of the stored operand matrix (M extent for a KC
+  // operand, K extent for an MC operand; rows beyond it read as zero).
+  // For an MC operand, a_row0 / b_row0 is the first column.
   // On return every wave has passed a barrier after its last LDS read, so the
   // LDS stages may be reused.
   __device__ __forceinline__ void run(const char* __restrict__ A, int64_t lda_bytes,
@@ -197,18 +292,37 @@ struct WideMma {
     const int wm = wave % WGM;
     const int wn = wave / WGM;
     zero();
-    const int nk = (int)(kbytes / kRowBytes);
-    const __amdgpu_buffer_rsrc_t ra = panel_rsrc(A, lda_bytes, a_row0, a_rows, BM);
-    const __amdgpu_buffer_rsrc_t rb = panel_rsrc(B, ldb_bytes, b_row0, b_rows, BN);
+    const int nk = (int)(kbytes / RB);
+    // KC operands: panel of BM (BN) rows, K position as scalar byte offset.
+    // MC operands: panel of BM (BN) columns, K position as scalar row offset.
+    const __amdgpu_buffer_rsrc_t ra = ALAY == kLayoutKC
+                                          ? panel_rsrc(A, lda_bytes, a_row0, a_rows, BM)
+                                          : panel_rsrc_mc(A, lda_bytes, a_row0, a_rows);
+    const __amdgpu_buffer_rsrc_t rb = BLAY == kLayoutKC
+                                          ? panel_rsrc(B, ldb_bytes, b_row0, b_rows, BN)
+                                          : panel_rsrc_mc(B, ldb_bytes, b_row0, b_rows);
     uint32_t offa[LA], offb[LB];
-    panel_offsets<LA>(lda_bytes, wave, lane, offa);
-    panel_offsets<LB>(ldb_bytes, wave, lane, offb);
+    if (ALAY == kLayoutKC)
+      panel_offsets<LA>(lda_bytes, wave, lane, offa);
+    else
+      panel_offsets_mc<BM, LA>(lda_bytes, wave, lane, offa);
+    if (BLAY == kLayoutKC)
+      panel_offsets<LB>(ldb_bytes, wave, lane, offb);
+    else
+      panel_offsets_mc<BN, LB>(ldb_bytes, wave, lane, offb);
+    // K position of tile t: KC operands move along the row (scalar offset);
+    // MC operands move down BK rows (per-lane offset, range-checked).
+    const uint32_t stepa = ALAY == kLayoutKC ? (uint32_t)RB : (uint32_t)(BK * lda_bytes);
+    const uint32_t stepb = BLAY == kLayoutKC ? (uint32_t)RB : (uint32_t)(BK * ldb_bytes);
 #pragma unroll
     for (int s = 0; s < STAGES - 1; ++s) {
       if (s < nk) {
         char* st = smem + s * kStageBytes;
-        issue_operand<LA>(ra, offa, s * kRowBytes, st, wave);
-        issue_operand<LB>(rb, offb, s * kRowBytes, st + BM * kRowBytes, wave);
+        const uint32_t ka = s * stepa, kb = s * stepb;
+        issue_operand<LA>(ra, offa, ALAY == kLayoutKC ? 0u : ka, ALAY == kLayoutKC ? (int)ka : 0, st,
+                          wave);
+        issue_operand<LB>(rb, offb, BLAY == kLayoutKC ? 0u : kb, BLAY == kLayoutKC ? (int)kb : 0,
+                          st + BM * RB, wave);
       }
     }
     for (int kt = 0; kt < nk; ++kt) {
@@ -225,11 +339,14 @@ struct WideMma {
       const int nt = kt + STAGES - 1;
       if (nt < nk) {
         char* st = smem + (nt % STAGES) * kStageBytes;
-        issue_operand<LA>(ra, offa, nt * kRowBytes, st, wave);
-        issue_operand<LB>(rb, offb, nt * kRowBytes, st + BM * kRowBytes, wave);
+        const uint32_t ka = nt * stepa, kb = nt * stepb;
+        issue_operand<LA>(ra, offa, ALAY == kLayoutKC ? 0u : ka, ALAY == kLayoutKC ? (int)ka : 0, st,
+                          wave);
+        issue_operand<LB>(rb, offb, BLAY == kLayoutKC ? 0u : kb, BLAY == kLayoutKC ? (int)kb : 0,
+                          st + BM * RB, wave);
       }
       const char* stage = smem + (kt % STAGES) * kStageBytes;
-      compute_stage(stage, stage + BM * kRowBytes, lane, wm, wn);
+      compute_stage(stage, stage + BM * RB, lane, wm, wn);
     }
     block_barrier();
   }

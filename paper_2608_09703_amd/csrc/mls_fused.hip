@@ -298,11 +298,9 @@ __global__ __launch_bounds__(Mma::NT, 1) void fused_bwd_kernel(FusedArgs a) {
 
 // Backward tile kernel of the wide bf16 core. Same arithmetic as
 // fused_bwd_kernel; the bf16 logit-gradient tile is staged in LDS as
-// [token][vocabulary] (rows of 512 bytes, 16-byte chunks XOR-swizzled with the
-// token index) and leaves the block as 16-byte coalesced stores: token-major
-// rows by plain copies, vocabulary-major rows through transposing LDS reads
-// (ds_read_b64_tr_b16: within a 16-lane group, lane j addresses row k0 + j/4,
-// column n0 + 4 (j % 4); lane i receives column n0 + i of rows k0 .. k0 + 3).
+// [token][vocabulary] (16-byte chunks XOR-swizzled with the token index) and
+// leaves the block as 16-byte coalesced stores of token-major slab rows. The
+// gradient GEMMs read this one layout for both products.
 template <class Mma, bool TAU1, int MINB>
 __global__ __launch_bounds__(Mma::NT, MINB) void fused_bwd_wide_kernel(FusedArgs a) {
   constexpr int BM = Mma::kBM;  // vocabulary rows
@@ -311,13 +309,11 @@ __global__ __launch_bounds__(Mma::NT, MINB) void fused_bwd_wide_kernel(FusedArgs
   constexpr int FM = Mma::FM;
   constexpr int FN = Mma::FN;
   constexpr int NT = Mma::NT;
-  constexpr int NWV = NT / 64;
   constexpr int kGRow = BM * 2;     // bytes per token row of the staged tile
   constexpr int kChunks = BM / 8;   // 16-byte chunks per token row
   constexpr int kCMask = kChunks - 1;
   static_assert((kChunks & kCMask) == 0 && kChunks <= 32, "row chunk count is a power of two");
   static_assert(BN * kGRow <= Mma::kSmemBytes, "staged tile fits in the stage memory");
-  typedef short v4s_t __attribute__((ext_vector_type(4)));
   __shared__ __attribute__((aligned(16))) char smem[Mma::kSmemBytes];
 
   const int tid = threadIdx.x;
@@ -407,7 +403,6 @@ __global__ __launch_bounds__(Mma::NT, MINB) void fused_bwd_wide_kernel(FusedArgs
 
     // 2. token-major slab: BN rows x kChunks chunks of 16 bytes
     uint16_t* slab = static_cast<uint16_t*>(a.slab) + (int64_t)i * a.T_pad * a.Vc;
-    uint16_t* slabT = static_cast<uint16_t*>(a.slabT) + (int64_t)i * a.T_pad * a.Vc;
 #pragma unroll 4
     for (int j = 0; j < BN * kChunks / NT; ++j) {
       const int idx = tid + NT * j;
@@ -415,32 +410,6 @@ __global__ __launch_bounds__(Mma::NT, MINB) void fused_bwd_wide_kernel(FusedArgs
       const int c = idx & kCMask;
       const uint4 v = *reinterpret_cast<const uint4*>(smem + t * kGRow + ((c ^ (t & kCMask)) << 4));
       *reinterpret_cast<uint4*>(slab + (tbase + t) * a.Vc + vloc + c * 8) = v;
-    }
-    // 3. vocabulary-major slab: BM rows x BN/8 chunks of 8 tokens, via transposing reads
-    {
-      const int grp = lane >> 4;
-      const int j16 = lane & 15;
-#pragma unroll 2
-      for (int it = 0; it < (BM / 16) * (BN / 8) / (4 * NWV); ++it) {
-        const int task = (it * NWV + wave) * 4 + grp;
-        const int vb = (task % (BM / 16)) * 16;
-        const int k0 = (task / (BM / 16)) * 8;
-        const int vv = vb + 4 * (j16 & 3);
-        const int ta = k0 + (j16 >> 2);
-        const int tb = ta + 4;
-        const int oa = ta * kGRow + (((vv >> 3) ^ (ta & kCMask)) << 4) + (vv & 7) * 2;
-        const int ob = tb * kGRow + (((vv >> 3) ^ (tb & kCMask)) << 4) + (vv & 7) * 2;
-        const v4s_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) v4s_t*)((__attribute__((address_space(3))) char*)smem + oa));
-        const v4s_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) v4s_t*)((__attribute__((address_space(3))) char*)smem + ob));
-        uint4 o;
-        o.x = (uint32_t)(uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16);
-        o.y = (uint32_t)(uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16);
-        o.z = (uint32_t)(uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16);
-        o.w = (uint32_t)(uint16_t)hi[2] | ((uint32_t)(uint16_t)hi[3] << 16);
-        *reinterpret_cast<uint4*>(slabT + (vloc + vb + j16) * a.T_pad + tbase + k0) = o;
-      }
     }
     block_barrier();  // the stage memory is reused by the next tile product
   }

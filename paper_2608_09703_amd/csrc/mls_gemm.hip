@@ -57,23 +57,48 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_nt_kernel(GemmArgs a) {
     }
 }
 
-// bf16 path: 256 x 256 tiles, 8 waves (2 per SIMD), direct-to-LDS loads; K is a
-// multiple of 64 (the callers pad it).
+// bf16 path: 256 x 256 tiles, 8 waves (2 per SIMD), direct-to-LDS loads, 4
+// stages of 32-wide K. The head chunk (grad_h) and the slab and h (grad_W) are
+// read in their stored layouts through transposing LDS reads, so no operand is
+// ever transposed in memory.
 constexpr int kWideBM = 256;
 constexpr int kWideBN = 256;
-constexpr int kWideThreads = 512;
+using WideGemmH = WideMma<kWideBM, kWideBN, 2, 4, 4, 64, kLayoutKC, kLayoutMC>;
+using WideGemmW = WideMma<kWideBM, kWideBN, 2, 4, 4, 64, kLayoutMC, kLayoutMC>;
 
-__global__ __launch_bounds__(kWideThreads, 2) void gemm_wide_kernel(GemmArgs a, int nb) {
-  using Mma = WideMma<kWideBM, kWideBN, 2, 4, 2>;
+template <class Mma>
+__device__ __forceinline__ void wide_tile(const GemmGroup& g, int tm, int tn, int64_t mext,
+                                          int64_t next, char* smem, int tid) {
   constexpr int FM = Mma::FM;
   constexpr int FN = Mma::FN;
-  __shared__ __attribute__((aligned(16))) char smem[Mma::kSmemBytes];
-
-  const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave % 2;
-  const int wn = wave / 2;
+  const int wm = wave % Mma::kWGM;
+  const int wn = wave / Mma::kWGM;
+  const int64_t m0 = (int64_t)tm * Mma::kBM;
+  const int64_t n0 = (int64_t)tn * Mma::kBN;
+  Mma mma;
+  mma.run(static_cast<const char*>(g.A), g.lda * 2, m0, g.rows, static_cast<const char*>(g.B),
+          g.ldb * 2, n0, g.cols, g.K * 2, smem, tid);
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      const int64_t n = n0 + Mma::col_of(wn, fn, lane);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t m = m0 + Mma::row_of(wm, fm, r, lane);
+        if (m < mext && n < next) {
+          float* c = g.C + m * g.ldc + n;
+          *c = g.accumulate ? *c + mma.acc[fm][fn][r] : mma.acc[fm][fn][r];
+        }
+      }
+    }
+}
+
+__global__ __launch_bounds__(WideGemmH::NT, 1) void gemm_wide_kernel(GemmArgs a, int nb) {
+  static_assert(WideGemmH::kSmemBytes == WideGemmW::kSmemBytes, "one LDS footprint");
+  __shared__ __attribute__((aligned(16))) char smem[WideGemmH::kSmemBytes];
   const int b = xcd_remap_phased(blockIdx.x, nb, a.phase_tiles);
   int gi = 0;
   for (int k = 1; k < a.ngroups; ++k)
@@ -87,27 +112,14 @@ __global__ __launch_bounds__(kWideThreads, 2) void gemm_wide_kernel(GemmArgs a, 
     tn = local % g.tiles_n;
     tm = local / g.tiles_n;
   }
-  const int64_t m0 = (int64_t)tm * kWideBM;
-  const int64_t n0 = (int64_t)tn * kWideBN;
-
-  Mma mma;
-  mma.run(static_cast<const char*>(g.A), g.lda * 2, m0, g.rows, static_cast<const char*>(g.B),
-          g.ldb * 2, n0, g.cols, g.K * 2, smem, tid);
-
-#pragma unroll
-  for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-    for (int fn = 0; fn < FN; ++fn) {
-      const int64_t n = n0 + Mma::col_of(wn, fn, lane);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t m = m0 + Mma::row_of(wm, fm, r, lane);
-        if (m < g.rows && n < g.cols) {
-          float* c = g.C + m * g.ldc + n;
-          *c = g.accumulate ? *c + mma.acc[fm][fn][r] : mma.acc[fm][fn][r];
-        }
-      }
-    }
+  // output extents: rows of C (grad_h: tokens; grad_W: chunk vocabulary rows),
+  // columns of C (the width); tiles_m * BM covers the former
+  const int64_t mext = g.kind == 0 ? g.rows : g.ldc_rows;
+  const int64_t next = g.ldc;
+  if (g.kind == 0)
+    wide_tile<WideGemmH>(g, tm, tn, mext, next, smem, threadIdx.x);
+  else
+    wide_tile<WideGemmW>(g, tm, tn, mext, next, smem, threadIdx.x);
 }
 
 template <typename S>
@@ -138,16 +150,18 @@ __global__ __launch_bounds__(kThreads) void transpose_kernel(TransposeArgs a) {
 
 }  // namespace
 
-int gemm_tile_rows(bool f32) { return f32 ? kGemmBM : kWideBM; }
-int gemm_tile_cols(bool f32) { return f32 ? kGemmBN : kWideBN; }
+int gemm_tile_rows(bool wide) { return wide ? kWideBM : kGemmBM; }
+int gemm_tile_cols(bool wide) { return wide ? kWideBN : kGemmBN; }
+
+hipError_t launch_gemm_wide(const GemmArgs& a, int total_tiles, hipStream_t stream) {
+  if (total_tiles <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gemm_wide_kernel, dim3(total_tiles), dim3(WideGemmH::NT), 0, stream, a,
+                     total_tiles);
+  return hipGetLastError();
+}
 
 hipError_t launch_gemm_nt(const GemmArgs& a, int total_tiles, bool f32, hipStream_t stream) {
   if (total_tiles <= 0) return hipSuccess;
-  if (!f32) {
-    hipLaunchKernelGGL(gemm_wide_kernel, dim3(total_tiles), dim3(kWideThreads), 0, stream, a,
-                       total_tiles);
-    return hipGetLastError();
-  }
   if (f32)
     hipLaunchKernelGGL(gemm_nt_kernel<F32>, dim3(total_tiles), dim3(kThreads), 0, stream, a);
   else

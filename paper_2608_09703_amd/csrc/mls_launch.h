@@ -76,6 +76,12 @@ struct GemmGroup {
   int32_t tile_begin;
   int32_t accumulate;
   int32_t group_m;  // tile order: 0 = n fastest; g > 0 = groups of g row tiles, rows fastest
+  // bf16 wide path only: operand layouts. 0: A is [m][k], B is [k][n] (grad_h:
+  // slab [t][v] times a head chunk [v][d]); 1: A is [k][m], B is [k][n] (grad_W:
+  // slab [t][v] as [k=t][m=v] times h [t][d]). rows/cols are the stored row counts
+  // of A/B for these layouts (see WideMma::run).
+  int32_t kind;
+  int64_t ldc_rows;  // grad_W (kind 1): rows of C to write (the chunk's vocabulary rows)
 };
 
 constexpr int kMaxGemmGroups = 2 * kMaxModels;
@@ -131,9 +137,11 @@ struct RowArgs {
 int fused_tile_rows(bool wide);
 hipError_t launch_fused_fwd(const FusedArgs& a, bool f32, hipStream_t stream);
 hipError_t launch_fused_bwd(const FusedArgs& a, bool f32, hipStream_t stream);
-// Output tile of the backward GEMMs for the given input dtype.
-int gemm_tile_rows(bool f32);
-int gemm_tile_cols(bool f32);
+// Output tile of the backward GEMMs (wide bf16 path or the general path).
+int gemm_tile_rows(bool wide);
+int gemm_tile_cols(bool wide);
+// Wide bf16 path: grad_h and grad_W products read in stored layouts.
+hipError_t launch_gemm_wide(const GemmArgs& a, int total_tiles, hipStream_t stream);
 hipError_t launch_gemm_nt(const GemmArgs& a, int total_tiles, bool f32, hipStream_t stream);
 hipError_t launch_transpose(const TransposeArgs& a, int64_t max_out_rows, int64_t max_cols,
                             bool f32, hipStream_t stream);
