@@ -98,13 +98,14 @@ __device__ __forceinline__ uint4 lds_read16_rb(const char* base, int row, int c)
 // in LDS as stored (K-tile rows of BM*2 bytes) and its fragments are read with
 // ds_read_b64_tr_b16, which hands lane i of each 16-lane group column m0+i of
 // four consecutive rows. Two such reads give the 8 consecutive K values of
-// one MFMA operand. Chunks of a staged row are XOR-swizzled with 2*(k % 4)
-// so the four rows one group reads fall in distinct banks.
+// one MFMA operand. Chunks of a staged row are XOR-swizzled with 4*(k % 4):
+// the 32 lanes served together read 64 contiguous bytes from each of four
+// rows, and the swizzle puts those four 64-byte pieces in distinct banks.
 enum { kLayoutKC = 0, kLayoutMC = 1 };
 
 typedef short v4s_t __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ int mc_chunk(int krow, int c) { return c ^ ((krow & 3) << 1); }
+__device__ __forceinline__ int mc_chunk(int krow, int c) { return c ^ ((krow & 3) << 2); }
 
 __device__ __forceinline__ uint2 lds_read_tr8(const char* p) {
   const v4s_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
