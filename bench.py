@@ -26,6 +26,34 @@ PEAK_FLOPS = {"bf16": 2.5e15, "f32": 157.3e12}  # MI355X dense MFMA peaks
 HBM_PEAK = 8.0e12
 
 
+def sources_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2608_09703_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        h.update(f.encode())
+        h.update(open(os.path.join(d, f), "rb").read())
+    return h.hexdigest()
+
+
+def profiled_traffic(workload, kernel):
+    """Per-launch HBM bytes of `kernel` from the committed rocprofv3 counter summary
+    (FETCH_SIZE + WRITE_SIZE scaled by a plain-copy calibration), or None when the
+    summary is missing or the kernel sources changed since it was taken."""
+    import re
+    path = os.path.join(ROOT, "profiles", f"{workload}_kernels.md")
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"```json\n(.*?)\n```", open(path).read(), re.S)
+    if not m:
+        return None
+    info = json.loads(m.group(1))
+    if info.get("sources_sha256") != sources_sha256():
+        return None
+    t = info.get("per_launch", {}).get(kernel)
+    return None if t is None else t["fetch_bytes"] + t["write_bytes"]
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -177,7 +205,7 @@ def main():
         "peak": peak / 1e12,
         "unit": "TFLOP/s",
         "frac": achieved / peak,
-        "traffic": None,
+        "traffic": profiled_traffic(name, dom),
     }
 
     if args.copy_mib > 0:
