@@ -25,4 +25,5 @@ from .mls_oracle import (  # noqa: F401
     grad_W_rows,
     n_valid,
     teacher_logq,
+    diagnostics,
 )

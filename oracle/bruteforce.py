@@ -101,3 +101,33 @@ def grads(h, W, labels, g_ce, g_kl, tau=1.0, teacher=None):
     gW = [[[math.fsum(G[i][t][v] * h[i][t][k] for t in range(T)) for k in range(len(h[i][0]))]
            for v in range(V)] for i in range(M)]
     return gh, gW
+
+
+def diagnostics(h, W, labels):
+    """Pairwise KL(p_i || p_j) and top-1 agreement, as loops (means over valid rows)."""
+    M = len(h)
+    L = [_logits(h[i], W[i]) for i in range(M)]
+    T = len(labels)
+    valid = [t for t in range(T) if labels[t] != IGNORE]
+    N = len(valid)
+    kl = [[[] for _ in range(M)] for _ in range(M)]
+    ag = [[0 for _ in range(M)] for _ in range(M)]
+    for t in valid:
+        P = [_softmax(L[i][t]) for i in range(M)]
+        top = []
+        for i in range(M):
+            best = 0
+            for v in range(1, len(L[i][t])):
+                if L[i][t][v] > L[i][t][best]:
+                    best = v
+            top.append(best)
+        for i in range(M):
+            for j in range(M):
+                if i != j:
+                    kl[i][j].append(math.fsum(P[i][v] * math.log(P[i][v] / P[j][v])
+                                              for v in range(len(P[i]))))
+                ag[i][j] += 1 if top[i] == top[j] else 0
+    if N == 0:
+        return [[0.0] * M for _ in range(M)], [[0.0] * M for _ in range(M)]
+    return ([[math.fsum(kl[i][j]) / N if i != j else 0.0 for j in range(M)] for i in range(M)],
+            [[ag[i][j] / N for j in range(M)] for i in range(M)])

@@ -341,3 +341,44 @@ def grad_W_rows(h, W, labels, vrows, g_ce, g_kl, tau=1.0, teacher=-1,
             G = _dlogits(tb, i, s, _f64(g_ce), _f64(g_kl), tau, N)
             out[i] += G[:, vrows].T @ _f64(h[i][rows])
     return out
+
+
+# ---------------------------------------------------------------------------
+# cross-model diagnostics (section 3, "Training Dynamics and Model Agreement";
+# appendix A plots the student-to-teacher direction)
+# ---------------------------------------------------------------------------
+
+def diagnostics(h, W, labels, ignore_index=IGNORE_INDEX):
+    """Pairwise KL divergence and top-1 next-token agreement between sub-models.
+
+    For every ordered pair (i, j), over the valid tokens t (label != ignore_index):
+      kl[i, j]    = mean_t KL(p_i[t] || p_j[t]),  p_i = softmax(l_i) at temperature 1
+      agree[i, j] = mean_t [argmax_v l_i[t] == argmax_v l_j[t]]
+    argmax ties go to the lowest vocabulary index. Returns a dict with kl[M, M],
+    agree[M, M], argmax[M, T] (of every token, valid or not) and n_valid; with
+    no valid token kl and agree are 0.
+    """
+    M, T, V, labels, _ = _check_problem(h, W, labels, None, ignore_index)
+    valid = labels != ignore_index
+    N = int(valid.sum())
+    kl_sum = np.zeros((M, M))
+    agree_sum = np.zeros((M, M))
+    argmax = np.zeros((M, T), dtype=np.int64)
+    for r0 in range(0, T, _ROW_BLOCK):
+        rows = np.arange(r0, min(T, r0 + _ROW_BLOCK))
+        L = [_f64(h[i][rows]) @ _f64(W[i]).T for i in range(M)]
+        logp = [Li - _logsumexp_rows(Li)[:, None] for Li in L]
+        am = [np.argmax(Li, axis=1) for Li in L]  # first maximum = lowest index
+        v = valid[rows]
+        for i in range(M):
+            argmax[i, rows] = am[i]
+            p = np.exp(logp[i])
+            for j in range(M):
+                if i != j:
+                    kl = (p * (logp[i] - logp[j])).sum(axis=1)
+                    kl_sum[i, j] += kl[v].sum()
+                agree_sum[i, j] += (am[i][v] == am[j][v]).sum()
+    den = N if N > 0 else 1
+    return {"kl": kl_sum / den if N else np.zeros((M, M)),
+            "agree": agree_sum / den if N else np.zeros((M, M)),
+            "argmax": argmax, "n_valid": N}

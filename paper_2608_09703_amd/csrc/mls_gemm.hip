@@ -93,12 +93,14 @@ __device__ __forceinline__ void wide_tile(const GemmGroup& g, int tm, int tn, in
           *c = g.accumulate ? *c + mma.acc[fm][fn][r] : mma.acc[fm][fn][r];
         }
       }
+      __builtin_amdgcn_sched_barrier(0);  // one 32x32 block of stores at a time
     }
 }
 
-__global__ __launch_bounds__(WideGemmH::NT, 1) void gemm_wide_kernel(GemmArgs a, int nb) {
-  static_assert(WideGemmH::kSmemBytes == WideGemmW::kSmemBytes, "one LDS footprint");
-  __shared__ __attribute__((aligned(16))) char smem[WideGemmH::kSmemBytes];
+template <class MmaH, class MmaW>
+__global__ __launch_bounds__(MmaH::NT, 1) void gemm_wide_kernel(GemmArgs a, int nb) {
+  static_assert(MmaH::kSmemBytes == MmaW::kSmemBytes && MmaH::NT == MmaW::NT, "one footprint");
+  __shared__ __attribute__((aligned(16))) char smem[MmaH::kSmemBytes];
   const int b = xcd_remap_phased(blockIdx.x, nb, a.phase_tiles);
   int gi = 0;
   for (int k = 1; k < a.ngroups; ++k)
@@ -112,14 +114,14 @@ __global__ __launch_bounds__(WideGemmH::NT, 1) void gemm_wide_kernel(GemmArgs a,
     tn = local % g.tiles_n;
     tm = local / g.tiles_n;
   }
-  // output extents: rows of C (grad_h: tokens; grad_W: chunk vocabulary rows),
-  // columns of C (the width); tiles_m * BM covers the former
-  const int64_t mext = g.kind == 0 ? g.rows : g.ldc_rows;
+  // output extents: rows of C (grad_h: tokens; grad_W: chunk vocabulary rows) and
+  // its columns (the width)
+  const int64_t mext = g.ldc_rows;
   const int64_t next = g.ldc;
   if (g.kind == 0)
-    wide_tile<WideGemmH>(g, tm, tn, mext, next, smem, threadIdx.x);
+    wide_tile<MmaH>(g, tm, tn, mext, next, smem, threadIdx.x);
   else
-    wide_tile<WideGemmW>(g, tm, tn, mext, next, smem, threadIdx.x);
+    wide_tile<MmaW>(g, tm, tn, mext, next, smem, threadIdx.x);
 }
 
 template <typename S>
@@ -155,8 +157,8 @@ int gemm_tile_cols(bool wide) { return wide ? kWideBN : kGemmBN; }
 
 hipError_t launch_gemm_wide(const GemmArgs& a, int total_tiles, hipStream_t stream) {
   if (total_tiles <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gemm_wide_kernel, dim3(total_tiles), dim3(WideGemmH::NT), 0, stream, a,
-                     total_tiles);
+  hipLaunchKernelGGL((gemm_wide_kernel<WideGemmH, WideGemmW>), dim3(total_tiles),
+                     dim3(WideGemmH::NT), 0, stream, a, total_tiles);
   return hipGetLastError();
 }
 

@@ -374,3 +374,62 @@ def test_sampled_row_helpers_agree_with_full():
     for i in range(M):
         np.testing.assert_allclose(ghr[i], gh[i][rows], rtol=1e-12, atol=1e-15)
         np.testing.assert_allclose(gWr[i], gW[i][[1, 9]], rtol=1e-12, atol=1e-15)
+
+
+# ----------------------------------------------------------------------------
+# cross-model diagnostics: pairwise KL and top-1 agreement
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", [61, 62])
+def test_diagnostics_bruteforce(seed):
+    M, T, dims, V = 3, 5, (2, 3, 2), 7
+    h, W, y = _problem(M, T, dims, V, seed=seed, ignore=(1,))
+    o = oracle.diagnostics(h, W, y)
+    kl, ag = bruteforce.diagnostics(_tolist(h), _tolist(W), y.tolist())
+    np.testing.assert_allclose(o["kl"], kl, rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(o["agree"], ag, rtol=0, atol=0)
+
+
+def test_diagnostics_invariants():
+    M, T, dims, V = 3, 40, (4, 5, 4), 23
+    h, W, y = _problem(M, T, dims, V, seed=63, ignore=(3, 9))
+    h[2] = h[0].copy()
+    W[2] = W[0].copy()
+    o = oracle.diagnostics(h, W, y)
+    assert np.all(np.diag(o["kl"]) == 0) and np.all(np.diag(o["agree"]) == 1)
+    assert np.all(o["kl"] >= -1e-15)
+    assert abs(o["kl"][0, 2]) < 1e-14 and abs(o["kl"][2, 0]) < 1e-14 and o["agree"][0, 2] == 1
+    assert o["kl"][0, 1] > 1e-3 and o["kl"][0, 1] != pytest.approx(o["kl"][1, 0], rel=1e-6)
+    # the training loss's KL(q || p_i) at tau = 1 is the teacher-to-student entry
+    f = oracle.forward(h, W, y, tau=1.0)
+    np.testing.assert_allclose(f["kl"][:2], o["kl"][2, :2], rtol=1e-12, atol=1e-15)
+
+
+def test_diagnostics_argmax_ties_to_lowest_index():
+    """Tied maxima: every head maps to the same logits for vocabulary rows 2 and 5."""
+    h = [np.array([[1.0], [2.0]]), np.array([[1.0], [-1.0]])]
+    W = [np.array([[0.0], [1.0], [3.0], [2.0], [0.5], [3.0]]),
+         np.array([[4.0], [0.0], [1.0], [4.0], [-1.0], [0.0]])]
+    y = np.array([0, 1])
+    o = oracle.diagnostics(h, W, y)
+    assert o["argmax"][0].tolist() == [2, 2]
+    assert o["argmax"][1].tolist() == [0, 4]
+    assert o["agree"][0, 1] == 0.0
+
+
+def test_diagnostics_torch_crosscheck():
+    torch = pytest.importorskip("torch")
+    F = torch.nn.functional
+    M, T, dims, V = 3, 16, (8, 12, 16), 29
+    h, W, y = _problem(M, T, dims, V, seed=64, ignore=(5,))
+    o = oracle.diagnostics(h, W, y)
+    v = torch.tensor(y != -100)
+    L = [torch.tensor(h[i]) @ torch.tensor(W[i]).T for i in range(M)]
+    lp = [F.log_softmax(x, dim=1)[v] for x in L]
+    for i in range(M):
+        for j in range(M):
+            if i != j:
+                ref = F.kl_div(lp[j], lp[i], log_target=True, reduction="sum").item() / int(v.sum())
+                assert o["kl"][i, j] == pytest.approx(ref, rel=1e-12)
+            agree = (L[i].argmax(dim=1)[v] == L[j].argmax(dim=1)[v]).double().mean().item()
+            assert o["agree"][i, j] == pytest.approx(agree, abs=1e-15)
