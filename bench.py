@@ -7,6 +7,10 @@ teacher-to-student KL, and the gradients grad_h_i and grad_W_i with the coeffici
 eq. (3). Prints one JSON line (see README of the build for the fields).
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+With --diagnostics a step is instead the monitoring pass of paper section 3:
+mls_distill_fwd (log-sum-exp rows and losses) + mls_diagnostics (pairwise KL at
+temperature 1 and top-1 agreement of every pair of sub-models).
 """
 
 from __future__ import annotations
@@ -22,6 +26,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "fused LM-head+CE+KL fwd+bwd tokens/s (M=3, V=50304); % of bf16 MFMA peak"
+METRIC_DIAG = "cross-model diagnostics (fused forward + pairwise KL/top-1 agreement) tokens/s"
 PEAK_FLOPS = {"bf16": 2.5e15, "f32": 157.3e12}  # MI355X dense MFMA peaks
 HBM_PEAK = 8.0e12
 
@@ -67,14 +72,17 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample rows (0 = auto)")
     ap.add_argument("--vocab-chunk", type=int, default=0)
+    ap.add_argument("--diagnostics", action="store_true",
+                    help="time the forward + pairwise diagnostics pass instead of fwd+bwd")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB (a known-size "
                          "kernel to calibrate HBM byte counters)")
     return ap.parse_args()
 
 
-def cpu_baseline(wl, h, W, y, g_ce, g_kl, rows_req):
-    """Times the float64 CPU oracle (forward + backward) on a sample of rows."""
+def cpu_baseline(wl, h, W, y, g_ce, g_kl, rows_req, diagnostics=False):
+    """Times the float64 CPU oracle (forward + backward, or forward + diagnostics)
+    on a sample of rows."""
     import numpy as np
     import oracle
 
@@ -92,7 +100,10 @@ def cpu_baseline(wl, h, W, y, g_ce, g_kl, rows_req):
         yn = yn_all[:nrows]
         t0 = time.perf_counter()
         oracle.forward(hn, Wn, yn, tau=wl.tau)
-        oracle.backward(hn, Wn, yn, g_ce, g_kl, tau=wl.tau)
+        if diagnostics:
+            oracle.diagnostics(hn, Wn, yn)
+        else:
+            oracle.backward(hn, Wn, yn, g_ce, g_kl, tau=wl.tau)
         return time.perf_counter() - t0
 
     if rows_req > 0:
@@ -113,7 +124,8 @@ def cpu_baseline(wl, h, W, y, g_ce, g_kl, rows_req):
         "unit": "tokens/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": f"float64 numpy oracle, forward + backward on the first {rows} of {wl.T} tokens "
+        "sample": f"float64 numpy oracle, forward + {'diagnostics' if diagnostics else 'backward'} "
+                  f"on the first {rows} of {wl.T} tokens "
                   f"at full V={wl.V} and widths {list(wl.dims)}; {dt:.1f} s",
     }
 
@@ -151,11 +163,16 @@ def main():
     st_ptr = buf.stats.data_ptr()
     gh_p = [x.data_ptr() for x in gh]
     gW_p = [x.data_ptr() for x in gW]
+    kl_pair = torch.empty(wl.M, wl.M, dtype=torch.float32, device=dev)
+    agree = torch.empty(wl.M, wl.M, dtype=torch.float32, device=dev)
 
     def step():
         B.distill_fwd(p, st_ptr, buf.ce.data_ptr(), buf.kl.data_ptr(), buf.entropy.data_ptr(),
                       ws_ptr, ws_n, sh)
-        B.distill_bwd(p, st_ptr, gce.data_ptr(), gkl.data_ptr(), gh_p, gW_p, ws_ptr, ws_n, sh)
+        if args.diagnostics:
+            B.diagnostics(p, st_ptr, kl_pair.data_ptr(), agree.data_ptr(), None, ws_ptr, ws_n, sh)
+        else:
+            B.distill_bwd(p, st_ptr, gce.data_ptr(), gkl.data_ptr(), gh_p, gW_p, ws_ptr, ws_n, sh)
 
     log(f"workspace {ws_n / 2**20:.0f} MiB, stats {buf.stats.numel() / 2**20:.1f} MiB")
     for k in range(args.warmup):
@@ -177,11 +194,12 @@ def main():
     ms_total = t0.elapsed_time(t1)
     ms_step = ms_total / args.steps
     tokens_per_s = wl.T / (ms_step / 1e3)
-    flops_step = wl.algorithmic_flops()
+    # forward + backward: 6*T*V*sum(d); forward + diagnostics: two 2*T*V*sum(d) passes
+    flops_step = wl.algorithmic_flops() * (2.0 / 3.0 if args.diagnostics else 1.0)
     peak = PEAK_FLOPS[wl.dtype]
     pct = flops_step / (ms_step / 1e3) / peak * 100.0
     log(f"{args.steps} steps: {ms_step:.3f} ms/step, {tokens_per_s:,.0f} tokens/s, "
-        f"{pct:.1f}% of {wl.dtype} MFMA peak (algorithmic 6*T*V*sum(d))")
+        f"{pct:.1f}% of {wl.dtype} MFMA peak (algorithmic)")
 
     # per-kernel times from the library's event timer over the timed region
     kernels = {}
@@ -194,7 +212,7 @@ def main():
     # dense work per step of each MFMA kernel: the forward and the recompute each
     # contract 2*T*V*sum(d); the gradient GEMM launch holds both head products
     one = 2.0 * wl.T * wl.V * sum(wl.dims)
-    dense = {"fused_fwd": one, "fused_bwd": one, "gemm_grads": 2.0 * one}
+    dense = {"fused_fwd": one, "fused_bwd": one, "gemm_grads": 2.0 * one, "diag_tiles": one}
     dom = max((k for k in kernels if k in dense), key=lambda k: kernels[k]["ms_per_step"])
     per_launch = dense[dom] / kernels[dom]["launches_per_step"]
     achieved = per_launch / (kernels[dom]["avg_launch_ms"] / 1e3)
@@ -220,11 +238,11 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample of rows")
-        cpu = cpu_baseline(wl, h, W, y, g_ce, g_kl, args.cpu_rows)
+        cpu = cpu_baseline(wl, h, W, y, g_ce, g_kl, args.cpu_rows, args.diagnostics)
         log(f"oracle: {cpu['value']:.2f} tokens/s on {cpu['cores']} threads")
 
     out = {
-        "metric": METRIC,
+        "metric": METRIC_DIAG if args.diagnostics else METRIC,
         "value": tokens_per_s,
         "unit": "tokens/s",
         "n_gpus": 1,

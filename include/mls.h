@@ -169,6 +169,23 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
                            void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Cross-model diagnostics (paper section 3, "Training Dynamics and Model
+ * Agreement"): for every ordered pair of sub-models (i, j), over the valid
+ * tokens (label != ignore_index, in range)
+ *   kl_pair[i*M + j] = mean KL(softmax(l_i) || softmax(l_j))   (temperature 1)
+ *   agree[i*M + j]   = mean [argmax_v l_i == argmax_v l_j]     (ties: lowest index)
+ * kl_pair and agree are device float32 [M*M]; argmax (device int32 [M][T], may be
+ * NULL) receives every token's top-1 index per sub-model. `stats` must come from
+ * mls_distill_fwd on the same inputs (its log-sum-exp rows are reused; tau and
+ * teacher do not matter here). The workspace of mls_query_sizes suffices.
+ * M must be at most 4 (MLS_UNSUPPORTED otherwise). With no valid token the
+ * outputs are 0. Asynchronous on stream.
+ */
+mls_status mls_diagnostics(const mls_problem* p, const void* stats, float* kl_pair, float* agree,
+                           int32_t* argmax, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/*
  * Host helper: loss coefficients of the objective (host arrays of length M).
  *   mode MLS_MODE_PAPER (eq. (3) summed over sub-models):
  *     student g_ce = w (1 - alpha), g_kl = w alpha tau^2; teacher g_ce = w, g_kl = 0

@@ -153,6 +153,35 @@ def distill(h_list: Sequence[torch.Tensor], W_list: Sequence[torch.Tensor], labe
     return _Distill.apply(labels, opts, *h_list, *W_list)
 
 
+def run_diagnostics(p: B.Problem, buf: Buffers, device, kl_pair: torch.Tensor, agree: torch.Tensor,
+                    argmax: Optional[torch.Tensor]) -> None:
+    """Pairwise diagnostics into caller tensors; ``buf.stats`` must hold this problem's forward."""
+    B.diagnostics(p, buf.stats.data_ptr(), kl_pair.data_ptr(), agree.data_ptr(),
+                  argmax.data_ptr() if argmax is not None else None, buf.workspace.data_ptr(),
+                  buf.workspace.numel(), _stream(device))
+
+
+@torch.no_grad()
+def diagnostics(h_list: Sequence[torch.Tensor], W_list: Sequence[torch.Tensor],
+                labels: torch.Tensor, *, ignore_index: int = -100, want_argmax: bool = False):
+    """Cross-model ``(kl[M, M], agree[M, M], argmax[M, T] or None)`` of the sub-model heads.
+
+    ``kl[i, j]`` is the mean over valid tokens of KL(p_i || p_j) at temperature 1 and
+    ``agree[i, j]`` the fraction of valid tokens whose top-1 predictions coincide.
+    Runs the fused forward (for the log-sum-exp rows) and then the pairwise pass.
+    """
+    p = make_problem(h_list, W_list, labels, ignore_index=ignore_index)
+    dev = h_list[0].device
+    buf = Buffers(p, dev)
+    forward(p, buf, dev)
+    M, T = len(h_list), h_list[0].shape[0]
+    kl = torch.empty(M, M, dtype=torch.float32, device=dev)
+    agree = torch.empty(M, M, dtype=torch.float32, device=dev)
+    am = torch.empty(M, T, dtype=torch.int32, device=dev) if want_argmax else None
+    run_diagnostics(p, buf, dev, kl, agree, am)
+    return kl, agree, am
+
+
 def coefficients(M: int, *, alpha: float, tau: float = 1.0, teacher: int = -1,
                  mode: str = "paper", weights: Optional[Sequence[float]] = None):
     """``(g_ce, g_kl)`` lists of eq. (3) (``mode="paper"``) or the additive form."""

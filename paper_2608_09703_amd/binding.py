@@ -38,6 +38,7 @@ EXPORTED = (
     "mls_query_sizes",
     "mls_distill_fwd",
     "mls_distill_bwd",
+    "mls_diagnostics",
     "mls_coeffs",
     "mls_read_stats_header",
     "mls_status_string",
@@ -96,6 +97,7 @@ def lib():
         L.mls_distill_fwd.argtypes = [P, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
         L.mls_distill_bwd.argtypes = [P, vp, vp, vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp,
                                       ctypes.c_size_t, vp]
+        L.mls_diagnostics.argtypes = [P, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
         L.mls_coeffs.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_float, ctypes.c_float,
                                  ctypes.c_int32, fp, fp, fp]
         L.mls_read_stats_header.argtypes = [P, vp, vp, ctypes.POINTER(ctypes.c_int32),
@@ -167,6 +169,12 @@ def distill_bwd(p: Problem, stats: int, g_ce: Optional[int], g_kl: Optional[int]
     arr_W = (ctypes.c_void_p * MAX_MODELS)(*[x or None for x in grad_W])
     check(lib().mls_distill_bwd(ctypes.byref(p), stats, g_ce, g_kl, arr_h, arr_W, ws, ws_bytes,
                                 stream), "mls_distill_bwd")
+
+
+def diagnostics(p: Problem, stats: int, kl_pair: int, agree: int, argmax: Optional[int], ws: int,
+                ws_bytes: int, stream: int):
+    check(lib().mls_diagnostics(ctypes.byref(p), stats, kl_pair, agree, argmax, ws, ws_bytes,
+                                stream), "mls_diagnostics")
 
 
 def coeffs(M: int, teacher: int = -1, alpha: float = 0.0, tau: float = 1.0,

@@ -101,6 +101,9 @@ struct Plan {
   size_t off_partials = 0, off_lab = 0, fwd_bytes = 0;
   // backward workspace
   size_t off_slab = 0, off_slabT = 0, off_hT = 0, off_WT = 0, bwd_bytes = 0;
+  // diagnostics workspace (vocabulary segments of the pairwise pass)
+  int n_vt_diag = 0, n_tt_diag = 0;
+  size_t off_dpart = 0, off_drow = 0, diag_bytes = 0;
   size_t ws_bytes = 0;
   size_t stats_bytes = 0;
   size_t header_off = 0;
@@ -183,7 +186,19 @@ void make_plan(const mls_problem* p, Plan& pl) {
     off = align256(off + (size_t)pl.sumd * pl.Vc * pl.es);
   }
   pl.bwd_bytes = off;
-  pl.ws_bytes = std::max(pl.fwd_bytes, pl.bwd_bytes);
+
+  // diagnostics: one record per (vocabulary tile, token)
+  if (pl.M <= kMaxDiagModels) {
+    pl.n_vt_diag = (int)((p->V + diag_tile_rows(pl.wide) - 1) / diag_tile_rows(pl.wide));
+    pl.n_tt_diag = (int)((p->T + diag_tile_cols(pl.wide) - 1) / diag_tile_cols(pl.wide));
+    off = 0;
+    pl.off_dpart = off;
+    off = align256(off + (size_t)pl.n_vt_diag * pl.T * diag_record_floats(pl.M) * sizeof(float));
+    pl.off_drow = off;
+    off = align256(off + (size_t)pl.T * 2 * pl.M * pl.M * sizeof(float));
+    pl.diag_bytes = off;
+  }
+  pl.ws_bytes = std::max(std::max(pl.fwd_bytes, pl.bwd_bytes), pl.diag_bytes);
 
   pl.header_off = (size_t)(4ll * pl.M * pl.T + pl.T) * sizeof(float);
   pl.stats_bytes = align256(pl.header_off + 2 * sizeof(int32_t));
@@ -546,6 +561,61 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
     }
     if (e != hipSuccess) return hip_fail(e, "gradient GEMM launch");
   }
+  return MLS_OK;
+}
+
+mls_status mls_diagnostics(const mls_problem* p, const void* stats, float* kl_pair, float* agree,
+                           int32_t* argmax, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+  g_last_error.clear();
+  mls_status st = validate(p);
+  if (st != MLS_OK) return st;
+  if (p->M > kMaxDiagModels)
+    return fail(MLS_UNSUPPORTED, "diagnostics support M <= %d, got %d", kMaxDiagModels, p->M);
+  if (!stats || !kl_pair || !agree || !workspace)
+    return fail(MLS_INVALID_ARG, "stats, kl_pair, agree and workspace must be non-NULL");
+  if (!aligned(stats, 16) || !aligned(workspace, 16) || !aligned(kl_pair, 4) || !aligned(agree, 4) ||
+      !aligned(argmax, 4))
+    return fail(MLS_INVALID_ARG, "misaligned stats / workspace / output pointer");
+  Plan pl;
+  make_plan(p, pl);
+  if (workspace_bytes < pl.diag_bytes)
+    return fail(MLS_WORKSPACE_TOO_SMALL, "diagnostics need %zu workspace bytes, got %zu",
+                pl.diag_bytes, workspace_bytes);
+  char* ws = static_cast<char*>(workspace);
+  DiagArgs a;
+  memset(&a, 0, sizeof(a));
+  a.M = pl.M;
+  for (int i = 0; i < pl.M; ++i) {
+    a.h[i] = p->h[i];
+    a.W[i] = p->W[i];
+    a.d[i] = p->d[i];
+  }
+  a.T = p->T;
+  a.V = p->V;
+  a.labels = p->labels;
+  a.ignore_index = p->ignore_index;
+  a.lse1 = static_cast<const float*>(stats);  // lse1[M][T] leads the statistics
+  a.n_tt = pl.n_tt_diag;
+  a.n_vt = pl.n_vt_diag;
+  a.group_v = 8;
+  a.partials = reinterpret_cast<float*>(ws + pl.off_dpart);
+  a.rowvals = reinterpret_cast<float*>(ws + pl.off_drow);
+  a.kl_pair = kl_pair;
+  a.agree = agree;
+  a.argmax = argmax;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  {
+    ProfScope ps("diag_tiles", s);
+    e = launch_diag_tiles(a, pl.f32, pl.wide, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "diagnostics tile launch");
+  {
+    ProfScope ps("diag_reduce", s);
+    e = launch_diag_reduce(a, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "diagnostics reduction launch");
   return MLS_OK;
 }
 

@@ -1,0 +1,344 @@
+// Cross-model diagnostics (paper section 3, "Training Dynamics and Model
+// Agreement"): for every ordered pair of sub-models (i, j), the mean over valid
+// tokens of KL(p_i || p_j) at temperature 1 and the rate at which their top-1
+// next-token predictions agree (argmax ties go to the lowest vocabulary index).
+//
+// One block owns one (vocabulary tile, token tile) pair, as the fused forward
+// does, and computes the logits tile of every sub-model (all M accumulator sets
+// stay in registers, M <= 4). Then, per logit:
+//   p_i = exp(l_i - lse_i)          (lse_i from the forward statistics)
+//   D_ij += p_i (l_i - l_j)         for every ordered pair i != j
+//   running argmax of l_i
+// and writes one record per token of the tile. Per token, after the records of
+// all vocabulary tiles are summed, KL(p_i || p_j) = D_ij - lse_i + lse_j. No
+// [T, V] tensor is formed.
+#include <math.h>
+
+#include "mls_core.h"
+#include "mls_device.h"
+#include "mls_launch.h"
+
+namespace mls {
+
+namespace {
+
+template <int MM>
+struct DiagRec {
+  static constexpr int kFloats = MM * MM + 2 * MM;  // D[MM][MM], best[MM], index[MM]
+};
+
+template <class Mma, typename E, int MM, int MINB>
+__global__ __launch_bounds__(Mma::NT, MINB) void diag_tile_kernel(DiagArgs a) {
+  constexpr int BM = Mma::kBM;
+  constexpr int BN = Mma::kBN;
+  constexpr int WGM = Mma::kWGM;
+  constexpr int FM = Mma::FM;
+  constexpr int FN = Mma::FN;
+  constexpr int REC = DiagRec<MM>::kFloats;
+  __shared__ __attribute__((aligned(16))) char smem[Mma::kSmemBytes];
+  __shared__ float red[WGM][BN][REC];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave % WGM;
+  const int wn = wave / WGM;
+  const int hi = lane >> 5;
+  const int bl = xcd_remap(blockIdx.x, gridDim.x);
+  int vt, tt;
+  tile_coords(bl, a.n_vt, a.n_tt, a.group_v, vt, tt);
+  const int64_t vbase = (int64_t)vt * BM;
+  const int64_t tbase = (int64_t)tt * BN;
+  const bool full = vbase + BM <= a.V;
+
+  Mma mma[MM];
+#pragma unroll
+  for (int j = 0; j < MM; ++j) {
+    const int64_t kb = a.d[j] * E::kBytes;
+    mma[j].run(static_cast<const char*>(a.W[j]), kb, vbase, a.V, static_cast<const char*>(a.h[j]),
+               kb, tbase, a.T, kb, smem, tid);
+  }
+
+#pragma unroll
+  for (int fn = 0; fn < FN; ++fn) {
+    const int64_t t = tbase + Mma::col_of(wn, fn, lane);
+    float lse[MM];
+#pragma unroll
+    for (int i = 0; i < MM; ++i) lse[i] = t < a.T ? a.lse1[(int64_t)i * a.T + t] * kLog2e : 0.f;
+    float D[MM][MM];
+    float best[MM];
+    int bidx[MM];
+#pragma unroll
+    for (int i = 0; i < MM; ++i) {
+      best[i] = -INFINITY;
+      bidx[i] = 0x7fffffff;
+#pragma unroll
+      for (int j = 0; j < MM; ++j) D[i][j] = 0.f;
+    }
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int v = (int)vbase + Mma::row_of(wm, fm, r, lane);
+        const bool ok = full || v < a.V;
+        float l[MM], p[MM];
+#pragma unroll
+        for (int i = 0; i < MM; ++i) {
+          l[i] = mma[i].acc[fm][fn][r];
+          p[i] = ok ? fast_exp2(fmaf(l[i], kLog2e, -lse[i])) : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < MM; ++i) {
+#pragma unroll
+          for (int j = 0; j < MM; ++j)
+            if (j != i) D[i][j] = fmaf(p[i], l[i] - l[j], D[i][j]);
+          // rows are visited in increasing order within a lane: strict > keeps the lowest
+          if (ok && l[i] > best[i]) {
+            best[i] = l[i];
+            bidx[i] = v;
+          }
+        }
+      }
+
+    // lanes l and l ^ 32 hold the same token column: combine, then the WGM
+    // waves of the column through LDS
+#pragma unroll
+    for (int i = 0; i < MM; ++i) {
+#pragma unroll
+      for (int j = 0; j < MM; ++j) D[i][j] += __shfl_xor(D[i][j], 32, 64);
+      const float ob = __shfl_xor(best[i], 32, 64);
+      const int oi = __shfl_xor(bidx[i], 32, 64);
+      if (ob > best[i] || (ob == best[i] && oi < bidx[i])) {
+        best[i] = ob;
+        bidx[i] = oi;
+      }
+    }
+    if (hi == 0) {
+      const int c = Mma::col_of(wn, fn, lane);
+#pragma unroll
+      for (int i = 0; i < MM; ++i) {
+#pragma unroll
+        for (int j = 0; j < MM; ++j) red[wm][c][i * MM + j] = D[i][j];
+        red[wm][c][MM * MM + i] = best[i];
+        red[wm][c][MM * MM + MM + i] = __int_as_float(bidx[i]);
+      }
+    }
+  }
+  __syncthreads();
+  // record layout [vocabulary tile][field][token]: consecutive threads write
+  // consecutive tokens
+  for (int idx = tid; idx < BN * (MM * MM + MM); idx += Mma::NT) {
+    const int c = idx % BN;
+    const int q = idx / BN;  // 0..MM*MM-1: D sums, MM*MM..: argmax
+    const int64_t t = tbase + c;
+    if (t >= a.T) continue;
+    float* out = a.partials + (int64_t)vt * REC * a.T;
+    if (q < MM * MM) {
+      float sum = 0.f;
+#pragma unroll
+      for (int w = 0; w < WGM; ++w) sum += red[w][c][q];
+      out[(int64_t)q * a.T + t] = sum;
+    } else {
+      const int i = q - MM * MM;
+      float b = red[0][c][MM * MM + i];
+      int bi = __float_as_int(red[0][c][MM * MM + MM + i]);
+#pragma unroll
+      for (int w = 1; w < WGM; ++w) {
+        const float ob = red[w][c][MM * MM + i];
+        const int oi = __float_as_int(red[w][c][MM * MM + MM + i]);
+        if (ob > b || (ob == b && oi < bi)) {
+          b = ob;
+          bi = oi;
+        }
+      }
+      out[(int64_t)(MM * MM + i) * a.T + t] = b;
+      out[(int64_t)(MM * MM + MM + i) * a.T + t] = __int_as_float(bi);
+    }
+  }
+}
+
+// Per token: sum the records of all vocabulary tiles, finish KL(p_i || p_j) and
+// the argmax, and write the per-token values the mean reduction reads. A block
+// takes kRowTok tokens; its kRowSlices thread rows each sum every kRowSlices-th
+// vocabulary tile, and the slices are combined in a fixed order.
+constexpr int kRowTok = 32;
+constexpr int kRowSlices = 8;
+
+template <int MM>
+__global__ __launch_bounds__(kRowTok * kRowSlices) void diag_rows_kernel(DiagArgs a) {
+  constexpr int REC = DiagRec<MM>::kFloats;
+  __shared__ float sh[kRowSlices][REC][kRowTok];
+  const int c = threadIdx.x % kRowTok;
+  const int g = threadIdx.x / kRowTok;
+  const int64_t t = (int64_t)blockIdx.x * kRowTok + c;
+  float D[MM * MM];
+  float best[MM];
+  int bidx[MM];
+#pragma unroll
+  for (int q = 0; q < MM * MM; ++q) D[q] = 0.f;
+#pragma unroll
+  for (int i = 0; i < MM; ++i) {
+    best[i] = -INFINITY;
+    bidx[i] = 0x7fffffff;
+  }
+  if (t < a.T) {
+    for (int vt = g; vt < a.n_vt; vt += kRowSlices) {
+      const float* in = a.partials + (int64_t)vt * REC * a.T + t;
+#pragma unroll
+      for (int q = 0; q < MM * MM; ++q) D[q] += in[(int64_t)q * a.T];
+#pragma unroll
+      for (int i = 0; i < MM; ++i) {
+        const float ob = in[(int64_t)(MM * MM + i) * a.T];
+        const int oi = __float_as_int(in[(int64_t)(MM * MM + MM + i) * a.T]);
+        if (ob > best[i] || (ob == best[i] && oi < bidx[i])) {
+          best[i] = ob;
+          bidx[i] = oi;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < MM * MM; ++q) sh[g][q][c] = D[q];
+#pragma unroll
+  for (int i = 0; i < MM; ++i) {
+    sh[g][MM * MM + i][c] = best[i];
+    sh[g][MM * MM + MM + i][c] = __int_as_float(bidx[i]);
+  }
+  __syncthreads();
+  if (g != 0 || t >= a.T) return;
+  for (int w = 1; w < kRowSlices; ++w) {
+#pragma unroll
+    for (int q = 0; q < MM * MM; ++q) D[q] += sh[w][q][c];
+#pragma unroll
+    for (int i = 0; i < MM; ++i) {
+      const float ob = sh[w][MM * MM + i][c];
+      const int oi = __float_as_int(sh[w][MM * MM + MM + i][c]);
+      if (ob > best[i] || (ob == best[i] && oi < bidx[i])) {
+        best[i] = ob;
+        bidx[i] = oi;
+      }
+    }
+  }
+  const int64_t y = a.labels[t];
+  const bool valid = y != a.ignore_index && y >= 0 && y < a.V;
+  float* row = a.rowvals + t * (2 * MM * MM);
+#pragma unroll
+  for (int i = 0; i < MM; ++i) {
+    const float li = a.lse1[(int64_t)i * a.T + t];
+#pragma unroll
+    for (int j = 0; j < MM; ++j) {
+      const float lj = a.lse1[(int64_t)j * a.T + t];
+      row[i * MM + j] = (valid && i != j) ? D[i * MM + j] - li + lj : 0.f;
+      row[MM * MM + i * MM + j] = (valid && bidx[i] == bidx[j]) ? 1.f : 0.f;
+    }
+    if (a.argmax) a.argmax[(int64_t)i * a.T + t] = bidx[i];
+  }
+}
+
+constexpr int kRedThreads = 1024;
+
+template <int MM>
+__global__ __launch_bounds__(kRedThreads) void diag_mean_kernel(DiagArgs a) {
+  constexpr int Q = 2 * MM * MM + 1;  // kl[MM][MM], agree[MM][MM], count
+  __shared__ double part[kRedThreads / 64][Q];
+  double acc[Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) acc[q] = 0.0;
+  for (int64_t t = threadIdx.x; t < a.T; t += kRedThreads) {
+    const int64_t y = a.labels[t];
+    if (y != a.ignore_index && y >= 0 && y < a.V) acc[Q - 1] += 1.0;
+    const float* row = a.rowvals + t * (2 * MM * MM);
+#pragma unroll
+    for (int q = 0; q < 2 * MM * MM; ++q) acc[q] += row[q];
+  }
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    double v = acc[q];
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    if (lane == 0) part[wave][q] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  double tot[Q];
+  for (int q = 0; q < Q; ++q) {
+    tot[q] = 0.0;
+    for (int w = 0; w < kRedThreads / 64; ++w) tot[q] += part[w][q];
+  }
+  const double n = tot[Q - 1];
+  const double inv = n > 0 ? 1.0 / n : 0.0;
+  for (int q = 0; q < MM * MM; ++q) {
+    a.kl_pair[q] = (float)(tot[q] * inv);
+    a.agree[q] = (float)(tot[MM * MM + q] * inv);
+  }
+}
+
+// All M accumulator sets of a tile stay live. Up to M = 3 the wide bf16 path
+// runs four waves of 64x64 (64 accumulators per lane per model) at two blocks
+// per CU; for M = 4 that no longer fits, and eight waves of 64x32 (32 per
+// model) share the 128x128 tile. The general path uses the four-wave
+// register-staged core on 128x64.
+using DiagWide = WideMma<kFusedWideBM, kDiagBN, 2, 2, 2>;
+using DiagWide8 = WideMma<kFusedWideBM, kDiagBN, 2, 4, 2>;
+template <typename E>
+using DiagGen = TileMma<E, kFusedBM, kDiagGenBN, 2, 2>;
+
+template <int MM>
+hipError_t launch_tiles_m(const DiagArgs& a, bool f32, bool wide, hipStream_t stream) {
+  const dim3 grid((unsigned)a.n_tt * (unsigned)a.n_vt);
+  if (f32)
+    hipLaunchKernelGGL((diag_tile_kernel<DiagGen<F32>, F32, MM, 2>), grid, dim3(kThreads), 0,
+                       stream, a);
+  else if (wide) {
+    if constexpr (MM <= 3)
+      hipLaunchKernelGGL((diag_tile_kernel<DiagWide, Bf16, MM, 2>), grid, dim3(DiagWide::NT), 0,
+                         stream, a);
+    else
+      hipLaunchKernelGGL((diag_tile_kernel<DiagWide8, Bf16, MM, 1>), grid, dim3(DiagWide8::NT), 0,
+                         stream, a);
+  }
+  else
+    hipLaunchKernelGGL((diag_tile_kernel<DiagGen<Bf16>, Bf16, MM, 2>), grid, dim3(kThreads), 0,
+                       stream, a);
+  return hipGetLastError();
+}
+
+template <int MM>
+hipError_t launch_reduce_m(const DiagArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(diag_rows_kernel<MM>, dim3((unsigned)((a.T + kRowTok - 1) / kRowTok)),
+                     dim3(kRowTok * kRowSlices), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(diag_mean_kernel<MM>, dim3(1), dim3(kRedThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int diag_tile_rows(bool wide) { return wide ? kFusedWideBM : kFusedBM; }
+int diag_tile_cols(bool wide) { return wide ? kDiagBN : kDiagGenBN; }
+int diag_record_floats(int M) { return M * M + 2 * M; }
+
+hipError_t launch_diag_tiles(const DiagArgs& a, bool f32, bool wide, hipStream_t stream) {
+  switch (a.M) {
+    case 1: return launch_tiles_m<1>(a, f32, wide, stream);
+    case 2: return launch_tiles_m<2>(a, f32, wide, stream);
+    case 3: return launch_tiles_m<3>(a, f32, wide, stream);
+    case 4: return launch_tiles_m<4>(a, f32, wide, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_diag_reduce(const DiagArgs& a, hipStream_t stream) {
+  switch (a.M) {
+    case 1: return launch_reduce_m<1>(a, stream);
+    case 2: return launch_reduce_m<2>(a, stream);
+    case 3: return launch_reduce_m<3>(a, stream);
+    case 4: return launch_reduce_m<4>(a, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace mls

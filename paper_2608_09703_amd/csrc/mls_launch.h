@@ -133,6 +133,30 @@ struct RowArgs {
   float* entropy;
 };
 
+// Cross-model diagnostics (M <= kMaxDiagModels).
+constexpr int kMaxDiagModels = 4;
+constexpr int kDiagBN = 128;     // token tile, wide bf16 path
+constexpr int kDiagGenBN = 64;   // token tile, general path
+struct DiagArgs {
+  int32_t M;
+  const void* h[kMaxModels];
+  const void* W[kMaxModels];
+  int64_t d[kMaxModels];
+  int64_t T;
+  int64_t V;
+  const int64_t* labels;
+  int64_t ignore_index;
+  const float* lse1;  // [M][T] from the forward statistics
+  int32_t n_tt;
+  int32_t n_vt;
+  int32_t group_v;        // tile order: vocabulary tiles per group
+  float* partials;        // [n_vt][M*M + 2M][T]
+  float* rowvals;         // [T][2*M*M]
+  float* kl_pair;         // [M][M]
+  float* agree;           // [M][M]
+  int32_t* argmax;        // [M][T] or null
+};
+
 // Launchers (each enqueues on `stream` and returns the launch status).
 int fused_tile_rows(bool wide);
 hipError_t launch_fused_fwd(const FusedArgs& a, bool f32, hipStream_t stream);
@@ -145,6 +169,11 @@ hipError_t launch_gemm_wide(const GemmArgs& a, int total_tiles, hipStream_t stre
 hipError_t launch_gemm_nt(const GemmArgs& a, int total_tiles, bool f32, hipStream_t stream);
 hipError_t launch_transpose(const TransposeArgs& a, int64_t max_out_rows, int64_t max_cols,
                             bool f32, hipStream_t stream);
+int diag_tile_rows(bool wide);
+int diag_tile_cols(bool wide);
+int diag_record_floats(int M);
+hipError_t launch_diag_tiles(const DiagArgs& a, bool f32, bool wide, hipStream_t stream);
+hipError_t launch_diag_reduce(const DiagArgs& a, hipStream_t stream);
 hipError_t launch_label_logits(const RowArgs& a, bool f32, hipStream_t stream);
 hipError_t launch_finalize_rows(const RowArgs& a, hipStream_t stream);
 hipError_t launch_reduce_losses(const RowArgs& a, hipStream_t stream);

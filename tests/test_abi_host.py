@@ -162,3 +162,24 @@ def test_chunk_width_is_rounded():
     p2 = _fake_problem(vocab_chunk=1024)
     ws2, _ = B.query_sizes(p2)
     assert ws1 == ws2
+
+
+def test_diagnostics_reject_bad_arguments_before_device_work():
+    fake = 1 << 40
+    out = fake + (1 << 30)
+    p = _fake_problem(M=5)
+    ws, _ = B.query_sizes(p)
+    with pytest.raises(B.MlsError) as e:  # more sub-models than the pairwise pass holds
+        B.diagnostics(p, fake, out, out + 256, None, fake + (1 << 20), ws, None)
+    assert e.value.status == B.MLS_UNSUPPORTED
+    p = _fake_problem()
+    ws, _ = B.query_sizes(p)
+    with pytest.raises(B.MlsError) as e:
+        B.diagnostics(p, fake, None, out, None, fake + (1 << 20), ws, None)
+    assert e.value.status == B.MLS_INVALID_ARG
+    with pytest.raises(B.MlsError) as e:
+        B.diagnostics(p, fake, out, out + 256, out + 513, fake + (1 << 20), ws, None)
+    assert e.value.status == B.MLS_INVALID_ARG  # misaligned argmax
+    with pytest.raises(B.MlsError) as e:
+        B.diagnostics(p, fake, out, out + 256, None, fake + (1 << 20), 16, None)
+    assert e.value.status == B.MLS_WORKSPACE_TOO_SMALL
