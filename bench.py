@@ -41,12 +41,13 @@ def sources_sha256():
     return h.hexdigest()
 
 
-def profiled_traffic(workload, kernel):
+def profiled_traffic(workload, kernel, diagnostics=False):
     """Per-launch HBM bytes of `kernel` from the committed rocprofv3 counter summary
     (FETCH_SIZE + WRITE_SIZE scaled by a plain-copy calibration), or None when the
     summary is missing or the kernel sources changed since it was taken."""
     import re
-    path = os.path.join(ROOT, "profiles", f"{workload}_kernels.md")
+    kind = "diagnostics" if diagnostics else "kernels"
+    path = os.path.join(ROOT, "profiles", f"{workload}_{kind}.md")
     if not os.path.exists(path):
         return None
     m = re.search(r"```json\n(.*?)\n```", open(path).read(), re.S)
@@ -223,7 +224,7 @@ def main():
         "peak": peak / 1e12,
         "unit": "TFLOP/s",
         "frac": achieved / peak,
-        "traffic": profiled_traffic(name, dom),
+        "traffic": profiled_traffic(name, dom, args.diagnostics),
     }
 
     if args.copy_mib > 0:
