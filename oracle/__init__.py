@@ -9,6 +9,7 @@ Modules
 -------
 ``mls_oracle``  vectorised float64 numpy implementation (forward losses,
                 per-row statistics, the exact gradient, loss coefficients).
+``junction``    the inter-model junction of eq. (1), forward and backward.
 ``bruteforce``  the same definitions written as pure-Python loops with
                 ``math.fsum``; only usable on tiny shapes. It shares no code
                 with ``mls_oracle`` and exists to pin it.
@@ -27,3 +28,4 @@ from .mls_oracle import (  # noqa: F401
     teacher_logq,
     diagnostics,
 )
+from . import junction  # noqa: F401,E402

@@ -131,3 +131,15 @@ def diagnostics(h, W, labels):
         return [[0.0] * M for _ in range(M)], [[0.0] * M for _ in range(M)]
     return ([[math.fsum(kl[i][j]) / N if i != j else 0.0 for j in range(M)] for i in range(M)],
             [[ag[i][j] / N for j in range(M)] for i in range(M)])
+
+
+def junction(o, e, prev_first=True):
+    """Eq. (1) as loops: each token's o rescaled to ||e|| and concatenated with e."""
+    out = []
+    for ot, et in zip(o, e):
+        no = math.sqrt(math.fsum(x * x for x in ot))
+        ne = math.sqrt(math.fsum(x * x for x in et))
+        r = ne / no if no > 0 and ne > 0 else 0.0
+        scaled = [x * r for x in ot]
+        out.append(scaled + list(et) if prev_first else list(et) + scaled)
+    return out
