@@ -11,6 +11,9 @@ eq. (3). Prints one JSON line (see README of the build for the fields).
 With --diagnostics a step is instead the monitoring pass of paper section 3:
 mls_distill_fwd (log-sum-exp rows and losses) + mls_diagnostics (pairwise KL at
 temperature 1 and top-1 agreement of every pair of sub-models).
+
+With --junction a step is the forward and backward of every inter-model junction
+(eq. (1)) of a suite (mls_junction_fwd + mls_junction_bwd per junction).
 """
 
 from __future__ import annotations
@@ -27,6 +30,7 @@ if ROOT not in sys.path:
 
 METRIC = "fused LM-head+CE+KL fwd+bwd tokens/s (M=3, V=50304); % of bf16 MFMA peak"
 METRIC_DIAG = "cross-model diagnostics (fused forward + pairwise KL/top-1 agreement) tokens/s"
+METRIC_JUNCTION = "inter-model junctions fwd+bwd tokens/s (every junction of the suite)"
 PEAK_FLOPS = {"bf16": 2.5e15, "f32": 157.3e12}  # MI355X dense MFMA peaks
 HBM_PEAK = 8.0e12
 
@@ -41,12 +45,12 @@ def sources_sha256():
     return h.hexdigest()
 
 
-def profiled_traffic(workload, kernel, diagnostics=False):
+def profiled_traffic(workload, kernel, kind=False):
     """Per-launch HBM bytes of `kernel` from the committed rocprofv3 counter summary
     (FETCH_SIZE + WRITE_SIZE scaled by a plain-copy calibration), or None when the
     summary is missing or the kernel sources changed since it was taken."""
     import re
-    kind = "diagnostics" if diagnostics else "kernels"
+    kind = {False: "kernels", True: "diagnostics"}.get(kind, kind)
     path = os.path.join(ROOT, "profiles", f"{workload}_{kind}.md")
     if not os.path.exists(path):
         return None
@@ -75,6 +79,8 @@ def parse():
     ap.add_argument("--vocab-chunk", type=int, default=0)
     ap.add_argument("--diagnostics", action="store_true",
                     help="time the forward + pairwise diagnostics pass instead of fwd+bwd")
+    ap.add_argument("--junction", action="store_true",
+                    help="time the inter-model junctions (forward + backward) instead")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB (a known-size "
                          "kernel to calibrate HBM byte counters)")
@@ -131,6 +137,134 @@ def cpu_baseline(wl, h, W, y, g_ce, g_kl, rows_req, diagnostics=False):
     }
 
 
+def junction_bytes(T, d_prev, d_fresh, act_bytes, grad_bytes):
+    """Algorithmic HBM bytes of one junction forward and one backward launch: every
+    operand read once and every result written once."""
+    w = d_prev + d_fresh
+    fwd = T * w * act_bytes + T * w * act_bytes                   # read o, e; write x
+    bwd = T * w * grad_bytes + T * w * act_bytes + T * w * grad_bytes  # read g_x, o, e; write g_o, g_e
+    return fwd, bwd
+
+
+def cpu_junction(wl, inputs, rows_req):
+    """Times the float64 oracle of every junction (forward + backward) on a sample of rows."""
+    import numpy as np
+    from oracle import junction as OJ
+    npi = [[x.float().cpu().numpy() for x in trio] for trio in inputs]
+
+    def run(nrows):
+        t0 = time.perf_counter()
+        for o, e, g in npi:
+            OJ.forward(o[:nrows], e[:nrows])
+            OJ.backward(o[:nrows], e[:nrows], g[:nrows])
+        return time.perf_counter() - t0
+
+    rows = rows_req if rows_req > 0 else 256
+    while True:
+        dt = run(rows)
+        log(f"oracle sample {rows} rows: {dt:.2f} s")
+        if rows_req > 0 or dt >= 10.0 or rows >= wl.T:
+            break
+        rows = int(min(wl.T, max(2 * rows, rows * 14.0 / max(dt, 1e-3))))
+    # elementwise numpy: one thread
+    return {"value": rows / dt, "unit": "tokens/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"float64 numpy oracle, forward + backward of every junction on the first "
+                      f"{rows} of {wl.T} tokens; {dt:.1f} s"}
+
+
+def main_junction(args):
+    import torch
+    from paper_2608_09703_amd import binding as B
+    from paper_2608_09703_amd import workloads as WL
+
+    name = args.workload or "c5_junctions"
+    wl = WL.JUNCTIONS[name]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(f"junction workload {name}: T={wl.T} widths={wl.dims} {wl.act_dtype}/{wl.grad_dtype}")
+    inputs = [WL.make_junction_inputs(wl, m, device=dev) for m in range(len(wl.junctions))]
+    ea = 2 if wl.act_dtype == "bf16" else 4
+    eg = 2 if wl.grad_dtype == "bf16" else 4
+    act_code = B.MLS_BF16 if wl.act_dtype == "bf16" else B.MLS_F32
+    grad_code = B.MLS_BF16 if wl.grad_dtype == "bf16" else B.MLS_F32
+    calls = []
+    fwd_bytes = bwd_bytes = 0
+    for (dp, df), (o, e, gx) in zip(wl.junctions, inputs):
+        j = B.make_junction(wl.T, dp, df, act_code, grad_code)
+        x = torch.empty(wl.T, dp + df, dtype=o.dtype, device=dev)
+        g_o = torch.empty(o.shape, dtype=gx.dtype, device=dev)
+        g_e = torch.empty(e.shape, dtype=gx.dtype, device=dev)
+        calls.append((j, o, e, gx, x, g_o, g_e))
+        fb, bb = junction_bytes(wl.T, dp, df, ea, eg)
+        fwd_bytes += fb
+        bwd_bytes += bb
+    sh = torch.cuda.current_stream(dev).cuda_stream
+
+    def step():
+        for j, o, e, gx, x, g_o, g_e in calls:
+            B.junction_fwd(j, o.data_ptr(), e.data_ptr(), x.data_ptr(), sh)
+        for j, o, e, gx, x, g_o, g_e in reversed(calls):
+            B.junction_bwd(j, o.data_ptr(), e.data_ptr(), gx.data_ptr(), g_o.data_ptr(),
+                           g_e.data_ptr(), sh)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    B.profile_enable(True)
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    stream = torch.cuda.current_stream(dev)
+    t0.record(stream)
+    for _ in range(args.steps):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    B.profile_enable(False)
+    prof = B.profile_report()
+    ms_step = t0.elapsed_time(t1) / args.steps
+    kernels = {}
+    for kname, (launches, tot) in prof.items():
+        kernels[kname] = {"launches_per_step": launches / args.steps, "ms_per_step": tot / args.steps,
+                          "avg_launch_ms": tot / launches}
+        log(f"  {kname:14s} {launches / args.steps:5.1f} launches/step {tot / args.steps:8.4f} ms/step")
+    per_step = {"junction_fwd": fwd_bytes, "junction_bwd": bwd_bytes}
+    dom = max(per_step, key=lambda k: kernels[k]["ms_per_step"])
+    achieved = per_step[dom] / (kernels[dom]["ms_per_step"] / 1e3)
+    log(f"{ms_step:.4f} ms/step; {dom}: {achieved / 1e9:.0f} GB/s of algorithmic bytes")
+    if args.copy_mib > 0:
+        src = torch.ones(args.copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_junction(wl, inputs, args.cpu_rows)
+    out = {
+        "metric": METRIC_JUNCTION,
+        "value": wl.T / (ms_step / 1e3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": f"{wl.act_dtype} activations, {wl.grad_dtype} gradients (fp32 reductions)",
+        "data": "synthetic (seeded Gaussian sub-model outputs, fresh embeddings and gradients)",
+        "config": {"workload": name, "T": wl.T, "widths": list(wl.dims), "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK,
+                     "traffic": profiled_traffic(name, dom, "junction")},
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -138,6 +272,8 @@ def main():
         print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not part "
                                    "of it (see the sharding design note)", "n_gpus": args.gpus}))
         sys.exit(2)
+    if args.junction:
+        return main_junction(args)
 
     import torch
     from paper_2608_09703_amd import binding as B

@@ -186,6 +186,57 @@ mls_status mls_diagnostics(const mls_problem* p, const void* stats, float* kl_pa
                            void* stream);
 
 /*
+ * Inter-model junction (paper section 2, "Inter-model Junction", eq. (1)):
+ * per token t, the output o[t] (width d_prev) of sub-model m is rescaled to
+ * the Euclidean norm of the fresh embedding e[t] (width d_fresh) of
+ * sub-model m+1, and the two are concatenated into x[t] (width
+ * d_prev + d_fresh):
+ *   s = ||e[t]|| / ||o[t]||,  x[t] = [s*o[t] | e[t]]   (MLS_JUNCTION_PREV_FIRST)
+ *                             x[t] = [e[t] | s*o[t]]   (MLS_JUNCTION_FRESH_FIRST)
+ * PREV_FIRST puts sub-model m's channels first, as the text after eq. (1)
+ * describes; FRESH_FIRST is the literal order of eq. (1). A zero norm gives
+ * s = 0. Norms and dot products are accumulated in fp32.
+ */
+enum mls_junction_layout {
+  MLS_JUNCTION_PREV_FIRST = 0,
+  MLS_JUNCTION_FRESH_FIRST = 1
+};
+enum mls_junction_flags {
+  MLS_JUNCTION_ACCUMULATE = 1u  /* backward: g_o += and g_e += instead of = */
+};
+typedef struct mls_junction {
+  int64_t T;           /* tokens, >= 1 */
+  int64_t d_prev;      /* width of o: a multiple of 8 in [8, 8192] */
+  int64_t d_fresh;     /* width of e: a multiple of 8 in [8, 8192] */
+  int32_t act_dtype;   /* mls_dtype of o, e and x */
+  int32_t grad_dtype;  /* mls_dtype of g_x, g_o and g_e */
+  int32_t layout;      /* mls_junction_layout */
+  uint32_t flags;      /* mls_junction_flags */
+} mls_junction;
+
+/*
+ * Forward: x = junction(o, e). o [T][d_prev], e [T][d_fresh] and x
+ * [T][d_prev + d_fresh] are row-major device arrays of act_dtype, 16-byte
+ * aligned; x must not overlap o or e. Asynchronous on stream.
+ */
+mls_status mls_junction_fwd(const mls_junction* j, const void* o, const void* e, void* x,
+                            void* stream);
+
+/*
+ * Backward: with g_x [T][d_prev + d_fresh] the gradient of a loss with
+ * respect to x (grad_dtype), writes
+ *   g_o = s * (g - (g.o) o / ||o||^2)
+ *   g_e = g_e0 + (g.o) / (||o|| ||e||) * e
+ * where g and g_e0 are the blocks of g_x on the rescaled and the fresh
+ * channels (ratio terms are 0 where a norm is 0). g_o [T][d_prev] and g_e
+ * [T][d_fresh] are grad_dtype, 16-byte aligned, and must not overlap the
+ * inputs; with MLS_JUNCTION_ACCUMULATE they are added to (the sum is formed
+ * in fp32 and stored once). o and e are the forward's inputs.
+ */
+mls_status mls_junction_bwd(const mls_junction* j, const void* o, const void* e, const void* g_x,
+                            void* g_o, void* g_e, void* stream);
+
+/*
  * Host helper: loss coefficients of the objective (host arrays of length M).
  *   mode MLS_MODE_PAPER (eq. (3) summed over sub-models):
  *     student g_ce = w (1 - alpha), g_kl = w alpha tau^2; teacher g_ce = w, g_kl = 0

@@ -182,6 +182,66 @@ def diagnostics(h_list: Sequence[torch.Tensor], W_list: Sequence[torch.Tensor],
     return kl, agree, am
 
 
+def _junction_desc(o, e, grad_dtype, layout, flags=0):
+    if o.device.type != "cuda" or e.device != o.device:
+        raise RuntimeError("the junction runs on the GPU only")
+    if o.dim() != 2 or e.dim() != 2 or o.shape[0] != e.shape[0] or o.dtype != e.dtype:
+        raise ValueError("o [T, d_prev] and e [T, d_fresh] must share T and dtype")
+    if not (o.is_contiguous() and e.is_contiguous()):
+        raise ValueError("o and e must be contiguous")
+    lay = {"prev_first": B.MLS_JUNCTION_PREV_FIRST, "fresh_first": B.MLS_JUNCTION_FRESH_FIRST}[layout]
+    return B.make_junction(o.shape[0], o.shape[1], e.shape[1], _dtype_code(o.dtype),
+                           _dtype_code(grad_dtype), lay, flags)
+
+
+def junction_forward(o: torch.Tensor, e: torch.Tensor, *, layout: str = "prev_first",
+                     out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Eq. (1): ``x = [o * ||e|| / ||o|| | e]`` per token (no autograd)."""
+    j = _junction_desc(o, e, o.dtype, layout)
+    x = out if out is not None else torch.empty(o.shape[0], o.shape[1] + e.shape[1],
+                                                 dtype=o.dtype, device=o.device)
+    B.junction_fwd(j, o.data_ptr(), e.data_ptr(), x.data_ptr(), _stream(o.device))
+    return x
+
+
+def junction_backward(o: torch.Tensor, e: torch.Tensor, g_x: torch.Tensor, *,
+                      layout: str = "prev_first", g_o: Optional[torch.Tensor] = None,
+                      g_e: Optional[torch.Tensor] = None, accumulate: bool = False):
+    """``(g_o, g_e)`` of the junction for the upstream gradient ``g_x`` (dtype of ``g_x``)."""
+    if not g_x.is_contiguous() or g_x.shape != (o.shape[0], o.shape[1] + e.shape[1]):
+        raise ValueError("g_x must be a contiguous [T, d_prev + d_fresh] tensor")
+    j = _junction_desc(o, e, g_x.dtype, layout, B.MLS_JUNCTION_ACCUMULATE if accumulate else 0)
+    if g_o is None:
+        g_o = torch.empty(o.shape, dtype=g_x.dtype, device=o.device)
+    if g_e is None:
+        g_e = torch.empty(e.shape, dtype=g_x.dtype, device=o.device)
+    for g in (g_o, g_e):
+        if g.dtype != g_x.dtype or not g.is_contiguous():
+            raise ValueError("g_o / g_e must be contiguous and of g_x's dtype")
+    B.junction_bwd(j, o.data_ptr(), e.data_ptr(), g_x.data_ptr(), g_o.data_ptr(), g_e.data_ptr(),
+                   _stream(o.device))
+    return g_o, g_e
+
+
+class _Junction(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, o, e, layout):
+        ctx.save_for_backward(o, e)
+        ctx.layout = layout
+        return junction_forward(o, e, layout=layout)
+
+    @staticmethod
+    def backward(ctx, g_x):
+        o, e = ctx.saved_tensors
+        g_o, g_e = junction_backward(o, e, g_x.contiguous(), layout=ctx.layout)
+        return g_o.to(o.dtype), g_e.to(e.dtype), None
+
+
+def junction(o: torch.Tensor, e: torch.Tensor, *, layout: str = "prev_first") -> torch.Tensor:
+    """Inter-model junction of eq. (1) with autograd through the HIP kernels."""
+    return _Junction.apply(o, e, layout)
+
+
 def coefficients(M: int, *, alpha: float, tau: float = 1.0, teacher: int = -1,
                  mode: str = "paper", weights: Optional[Sequence[float]] = None):
     """``(g_ce, g_kl)`` lists of eq. (3) (``mode="paper"``) or the additive form."""

@@ -29,6 +29,10 @@ MLS_F32 = 1
 MLS_MODE_PAPER = 0
 MLS_MODE_ADDITIVE = 1
 
+MLS_JUNCTION_PREV_FIRST = 0
+MLS_JUNCTION_FRESH_FIRST = 1
+MLS_JUNCTION_ACCUMULATE = 1
+
 MLS_ACCUMULATE_GRAD_W = 1
 MLS_ACCUMULATE_GRAD_H = 2
 
@@ -39,6 +43,8 @@ EXPORTED = (
     "mls_distill_fwd",
     "mls_distill_bwd",
     "mls_diagnostics",
+    "mls_junction_fwd",
+    "mls_junction_bwd",
     "mls_coeffs",
     "mls_read_stats_header",
     "mls_status_string",
@@ -79,6 +85,18 @@ class Problem(ctypes.Structure):
     ]
 
 
+class Junction(ctypes.Structure):
+    _fields_ = [
+        ("T", ctypes.c_int64),
+        ("d_prev", ctypes.c_int64),
+        ("d_fresh", ctypes.c_int64),
+        ("act_dtype", ctypes.c_int32),
+        ("grad_dtype", ctypes.c_int32),
+        ("layout", ctypes.c_int32),
+        ("flags", ctypes.c_uint32),
+    ]
+
+
 _lib = None
 
 
@@ -98,6 +116,9 @@ def lib():
         L.mls_distill_bwd.argtypes = [P, vp, vp, vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp,
                                       ctypes.c_size_t, vp]
         L.mls_diagnostics.argtypes = [P, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        J = ctypes.POINTER(Junction)
+        L.mls_junction_fwd.argtypes = [J, vp, vp, vp, vp]
+        L.mls_junction_bwd.argtypes = [J, vp, vp, vp, vp, vp, vp]
         L.mls_coeffs.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_float, ctypes.c_float,
                                  ctypes.c_int32, fp, fp, fp]
         L.mls_read_stats_header.argtypes = [P, vp, vp, ctypes.POINTER(ctypes.c_int32),
@@ -175,6 +196,23 @@ def diagnostics(p: Problem, stats: int, kl_pair: int, agree: int, argmax: Option
                 ws_bytes: int, stream: int):
     check(lib().mls_diagnostics(ctypes.byref(p), stats, kl_pair, agree, argmax, ws, ws_bytes,
                                 stream), "mls_diagnostics")
+
+
+def make_junction(T: int, d_prev: int, d_fresh: int, act_dtype: int = MLS_BF16,
+                  grad_dtype: int = MLS_F32, layout: int = MLS_JUNCTION_PREV_FIRST,
+                  flags: int = 0) -> Junction:
+    j = Junction()
+    j.T, j.d_prev, j.d_fresh = T, d_prev, d_fresh
+    j.act_dtype, j.grad_dtype, j.layout, j.flags = act_dtype, grad_dtype, layout, flags
+    return j
+
+
+def junction_fwd(j: Junction, o: int, e: int, x: int, stream: int):
+    check(lib().mls_junction_fwd(ctypes.byref(j), o, e, x, stream), "mls_junction_fwd")
+
+
+def junction_bwd(j: Junction, o: int, e: int, g_x: int, g_o: int, g_e: int, stream: int):
+    check(lib().mls_junction_bwd(ctypes.byref(j), o, e, g_x, g_o, g_e, stream), "mls_junction_bwd")
 
 
 def coeffs(M: int, teacher: int = -1, alpha: float = 0.0, tau: float = 1.0,

@@ -619,6 +619,114 @@ mls_status mls_diagnostics(const mls_problem* p, const void* stats, float* kl_pa
   return MLS_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+mls_status validate_junction(const mls_junction* j) {
+  if (!j) return fail(MLS_INVALID_ARG, "junction is NULL");
+  if (j->T < 1 || j->T > (1ll << 31)) return fail(MLS_INVALID_ARG, "T=%lld out of range", (long long)j->T);
+  const int64_t wmax = junction_max_width();
+  if (j->d_prev < 8 || j->d_fresh < 8 || j->d_prev > wmax || j->d_fresh > wmax)
+    return fail(MLS_UNSUPPORTED, "junction widths %lld / %lld outside [8, %lld]", (long long)j->d_prev,
+                (long long)j->d_fresh, (long long)wmax);
+  if (j->d_prev % 8 || j->d_fresh % 8)
+    return fail(MLS_UNSUPPORTED, "junction widths %lld / %lld are not multiples of 8",
+                (long long)j->d_prev, (long long)j->d_fresh);
+  if ((j->act_dtype != MLS_BF16 && j->act_dtype != MLS_F32) ||
+      (j->grad_dtype != MLS_BF16 && j->grad_dtype != MLS_F32))
+    return fail(MLS_UNSUPPORTED, "junction dtypes %d / %d unsupported", j->act_dtype, j->grad_dtype);
+  if (j->layout != MLS_JUNCTION_PREV_FIRST && j->layout != MLS_JUNCTION_FRESH_FIRST)
+    return fail(MLS_INVALID_ARG, "junction layout %d unknown", j->layout);
+  if (j->flags & ~(uint32_t)MLS_JUNCTION_ACCUMULATE)
+    return fail(MLS_INVALID_ARG, "unknown junction flags 0x%x", j->flags);
+  return MLS_OK;
+}
+
+bool disjoint(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x + na <= y || y + nb <= x;
+}
+
+JunctionArgs junction_args(const mls_junction* j) {
+  JunctionArgs a;
+  memset(&a, 0, sizeof(a));
+  a.T = j->T;
+  a.d_prev = j->d_prev;
+  a.d_fresh = j->d_fresh;
+  a.prev_first = j->layout == MLS_JUNCTION_PREV_FIRST;
+  a.accumulate = (j->flags & MLS_JUNCTION_ACCUMULATE) ? 1 : 0;
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+mls_status mls_junction_fwd(const mls_junction* j, const void* o, const void* e, void* x,
+                            void* stream) {
+  g_last_error.clear();
+  mls_status st = validate_junction(j);
+  if (st != MLS_OK) return st;
+  if (!o || !e || !x) return fail(MLS_INVALID_ARG, "o, e and x must be non-NULL");
+  if (!aligned(o, 16) || !aligned(e, 16) || !aligned(x, 16))
+    return fail(MLS_INVALID_ARG, "o, e and x must be 16-byte aligned");
+  const size_t es = j->act_dtype == MLS_F32 ? 4 : 2;
+  const size_t nx = (size_t)j->T * (j->d_prev + j->d_fresh) * es;
+  if (!disjoint(x, nx, o, (size_t)j->T * j->d_prev * es) ||
+      !disjoint(x, nx, e, (size_t)j->T * j->d_fresh * es))
+    return fail(MLS_INVALID_ARG, "x overlaps o or e");
+  JunctionArgs a = junction_args(j);
+  a.o = o;
+  a.e = e;
+  a.x = x;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t err;
+  {
+    ProfScope ps("junction_fwd", s);
+    err = launch_junction_fwd(a, j->act_dtype == MLS_F32, s);
+  }
+  if (err != hipSuccess) return hip_fail(err, "junction forward launch");
+  return MLS_OK;
+}
+
+mls_status mls_junction_bwd(const mls_junction* j, const void* o, const void* e, const void* g_x,
+                            void* g_o, void* g_e, void* stream) {
+  g_last_error.clear();
+  mls_status st = validate_junction(j);
+  if (st != MLS_OK) return st;
+  if (!o || !e || !g_x || !g_o || !g_e)
+    return fail(MLS_INVALID_ARG, "o, e, g_x, g_o and g_e must be non-NULL");
+  if (!aligned(o, 16) || !aligned(e, 16) || !aligned(g_x, 16) || !aligned(g_o, 16) || !aligned(g_e, 16))
+    return fail(MLS_INVALID_ARG, "junction operands must be 16-byte aligned");
+  const size_t ea = j->act_dtype == MLS_F32 ? 4 : 2;
+  const size_t eg = j->grad_dtype == MLS_F32 ? 4 : 2;
+  const size_t T = (size_t)j->T;
+  const size_t n_o = T * j->d_prev * ea, n_e = T * j->d_fresh * ea;
+  const size_t n_gx = T * (j->d_prev + j->d_fresh) * eg;
+  const size_t n_go = T * j->d_prev * eg, n_ge = T * j->d_fresh * eg;
+  const void* ins[3] = {o, e, g_x};
+  const size_t nin[3] = {n_o, n_e, n_gx};
+  for (int i = 0; i < 3; ++i)
+    if (!disjoint(g_o, n_go, ins[i], nin[i]) || !disjoint(g_e, n_ge, ins[i], nin[i]))
+      return fail(MLS_INVALID_ARG, "g_o / g_e overlap an input");
+  if (!disjoint(g_o, n_go, g_e, n_ge)) return fail(MLS_INVALID_ARG, "g_o and g_e overlap");
+  JunctionArgs a = junction_args(j);
+  a.o = o;
+  a.e = e;
+  a.g_x = g_x;
+  a.g_o = g_o;
+  a.g_e = g_e;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t err;
+  {
+    ProfScope ps("junction_bwd", s);
+    err = launch_junction_bwd(a, j->act_dtype == MLS_F32, j->grad_dtype == MLS_F32, s);
+  }
+  if (err != hipSuccess) return hip_fail(err, "junction backward launch");
+  return MLS_OK;
+}
+
 mls_status mls_read_stats_header(const mls_problem* p, const void* stats, void* stream,
                                  int32_t* n_valid, int32_t* device_flags) {
   g_last_error.clear();

@@ -157,6 +157,21 @@ struct DiagArgs {
   int32_t* argmax;        // [M][T] or null
 };
 
+// Inter-model junction (eq. (1)).
+struct JunctionArgs {
+  int64_t T;
+  int64_t d_prev;   // width of o
+  int64_t d_fresh;  // width of e
+  int32_t prev_first;
+  int32_t accumulate;
+  const void* o;    // [T][d_prev]
+  const void* e;    // [T][d_fresh]
+  void* x;          // [T][d_prev + d_fresh]
+  const void* g_x;  // [T][d_prev + d_fresh]
+  void* g_o;        // [T][d_prev]
+  void* g_e;        // [T][d_fresh]
+};
+
 // Launchers (each enqueues on `stream` and returns the launch status).
 int fused_tile_rows(bool wide);
 hipError_t launch_fused_fwd(const FusedArgs& a, bool f32, hipStream_t stream);
@@ -174,6 +189,10 @@ int diag_tile_cols(bool wide);
 int diag_record_floats(int M);
 hipError_t launch_diag_tiles(const DiagArgs& a, bool f32, bool wide, hipStream_t stream);
 hipError_t launch_diag_reduce(const DiagArgs& a, hipStream_t stream);
+bool junction_shape(int64_t width, int* tpr, int* cpl);
+int64_t junction_max_width();
+hipError_t launch_junction_fwd(const JunctionArgs& a, bool act_f32, hipStream_t stream);
+hipError_t launch_junction_bwd(const JunctionArgs& a, bool act_f32, bool grad_f32, hipStream_t stream);
 hipError_t launch_label_logits(const RowArgs& a, bool f32, hipStream_t stream);
 hipError_t launch_finalize_rows(const RowArgs& a, hipStream_t stream);
 hipError_t launch_reduce_losses(const RowArgs& a, hipStream_t stream);

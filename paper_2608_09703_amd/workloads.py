@@ -111,3 +111,58 @@ def make_inputs(wl: Workload, device="cpu", seed: Optional[int] = None):
 def custom(M: int, T: int, dims: Sequence[int], V: int, dtype="bf16", **kw) -> Workload:
     """A workload of arbitrary shape (for parity tests below full size)."""
     return Workload(kw.pop("name", f"custom_m{M}_t{T}_v{V}"), M, T, tuple(dims), V, dtype, **kw)
+
+
+# ---------------------------------------------------------------------------
+# inter-model junction inputs
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class JunctionWorkload:
+    """Inputs of the junctions between consecutive sub-models of one suite.
+
+    Junction m joins sub-model m (output width ``dims[m]``) and m+1 (fresh
+    embedding width ``dims[m+1] - dims[m]``). Sub-model outputs are drawn
+    N(0, o_std^2) and fresh embeddings N(0, e_std^2): transformer outputs have
+    much larger norms than input embeddings (the mismatch the junction's
+    rescaling addresses). Upstream gradients are N(0, g_std^2).
+    """
+
+    name: str
+    T: int
+    dims: Tuple[int, ...]
+    act_dtype: str = "bf16"
+    grad_dtype: str = "f32"
+    o_std: float = 8.0
+    e_std: float = 0.02
+    g_std: float = 1e-3
+    seed: int = 0
+
+    @property
+    def junctions(self):
+        return [(self.dims[m], self.dims[m + 1] - self.dims[m]) for m in range(len(self.dims) - 1)]
+
+
+JUNCTIONS = {
+    "c2_junctions": JunctionWorkload("c2_junctions", 4096, (1024, 2048, 3072), seed=2002),
+    "c5_junctions": JunctionWorkload("c5_junctions", 32768, (1536, 3072, 4608), seed=2005),
+    "paper3b_junctions": JunctionWorkload("paper3b_junctions", 4096, (1024, 2304, 4352), seed=2006),
+}
+
+
+def _dt(name):
+    return torch.bfloat16 if name == "bf16" else torch.float32
+
+
+def make_junction_inputs(wl: JunctionWorkload, m: int, device="cpu", seed: Optional[int] = None,
+                         T: Optional[int] = None):
+    """``(o, e, g_x)`` of junction ``m``; draw order o, e, g_x from one generator."""
+    d_prev, d_fresh = wl.junctions[m]
+    T = wl.T if T is None else T
+    g = torch.Generator(device=device)
+    g.manual_seed((wl.seed if seed is None else seed) * 16 + m)
+    o = (torch.randn(T, d_prev, generator=g, device=device) * wl.o_std).to(_dt(wl.act_dtype))
+    e = (torch.randn(T, d_fresh, generator=g, device=device) * wl.e_std).to(_dt(wl.act_dtype))
+    gx = (torch.randn(T, d_prev + d_fresh, generator=g, device=device) * wl.g_std).to(
+        _dt(wl.grad_dtype))
+    return o, e, gx

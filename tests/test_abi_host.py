@@ -39,25 +39,26 @@ def test_version_and_status_strings():
     assert L.mls_status_string(B.MLS_WORKSPACE_TOO_SMALL) == b"workspace too small"
 
 
-def test_problem_struct_layout_matches_header(tmp_path):
-    """The ctypes mirror of mls_problem has the C compiler's layout."""
+@pytest.mark.parametrize("cname,cls", [("mls_problem", B.Problem), ("mls_junction", B.Junction)])
+def test_struct_layout_matches_header(tmp_path, cname, cls):
+    """The ctypes mirrors of the C structs have the C compiler's layout."""
     import shutil
     import subprocess
     cc = shutil.which("gcc") or shutil.which("cc")
     if cc is None:
         pytest.skip("no C compiler")
-    fields = [f[0] for f in B.Problem._fields_]
+    fields = [f[0] for f in cls._fields_]
     prog = tmp_path / "layout.c"
-    body = "".join(f'printf("%zu\\n", offsetof(mls_problem, {f}));' for f in fields)
+    body = "".join(f'printf("%zu\\n", offsetof({cname}, {f}));' for f in fields)
     prog.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "mls.h"\n'
-                    'int main(void){printf("%zu\\n", sizeof(mls_problem));' + body + 'return 0;}')
+                    f'int main(void){{printf("%zu\\n", sizeof({cname}));' + body + 'return 0;}')
     exe = tmp_path / "layout"
     subprocess.run([cc, "-I", os.path.join(ROOT, "include"), str(prog), "-o", str(exe)], check=True)
     out = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True,
                                           check=True).stdout.split()]
-    assert out[0] == ctypes.sizeof(B.Problem)
+    assert out[0] == ctypes.sizeof(cls)
     for f, off in zip(fields, out[1:]):
-        assert getattr(B.Problem, f).offset == off, f
+        assert getattr(cls, f).offset == off, f
 
 
 @pytest.mark.parametrize("mode", [B.MLS_MODE_PAPER, B.MLS_MODE_ADDITIVE])
@@ -183,3 +184,44 @@ def test_diagnostics_reject_bad_arguments_before_device_work():
     with pytest.raises(B.MlsError) as e:
         B.diagnostics(p, fake, out, out + 256, None, fake + (1 << 20), 16, None)
     assert e.value.status == B.MLS_WORKSPACE_TOO_SMALL
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("T", 0, B.MLS_INVALID_ARG),
+    ("d_prev", 12, B.MLS_UNSUPPORTED),
+    ("d_fresh", 0, B.MLS_UNSUPPORTED),
+    ("d_prev", 8200, B.MLS_UNSUPPORTED),
+    ("act_dtype", 5, B.MLS_UNSUPPORTED),
+    ("grad_dtype", 5, B.MLS_UNSUPPORTED),
+    ("layout", 2, B.MLS_INVALID_ARG),
+    ("flags", 4, B.MLS_INVALID_ARG),
+])
+def test_junction_rejects_bad_descriptors_before_device_work(field, value, status):
+    j = B.make_junction(4096, 1024, 1024)
+    setattr(j, field, value)
+    fake = 1 << 40
+    with pytest.raises(B.MlsError) as e:
+        B.junction_fwd(j, fake, fake + (1 << 30), fake + (2 << 30), None)
+    assert e.value.status == status
+    with pytest.raises(B.MlsError) as e:
+        B.junction_bwd(j, fake, fake + (1 << 30), fake + (2 << 30), fake + (3 << 30),
+                       fake + (4 << 30), None)
+    assert e.value.status == status
+
+
+def test_junction_rejects_bad_pointers_before_device_work():
+    j = B.make_junction(4096, 1024, 1024)
+    fake = 1 << 40
+    with pytest.raises(B.MlsError) as e:  # misaligned
+        B.junction_fwd(j, fake + 8, fake + (1 << 30), fake + (2 << 30), None)
+    assert e.value.status == B.MLS_INVALID_ARG
+    with pytest.raises(B.MlsError) as e:  # x overlapping o
+        B.junction_fwd(j, fake, fake + (1 << 30), fake + 4096, None)
+    assert e.value.status == B.MLS_INVALID_ARG
+    with pytest.raises(B.MlsError) as e:  # g_o overlapping g_x
+        B.junction_bwd(j, fake, fake + (1 << 30), fake + (2 << 30), fake + (2 << 30) + 256,
+                       fake + (4 << 30), None)
+    assert e.value.status == B.MLS_INVALID_ARG
+    with pytest.raises(B.MlsError) as e:
+        B.junction_bwd(j, fake, None, fake + (2 << 30), fake + (3 << 30), fake + (4 << 30), None)
+    assert e.value.status == B.MLS_INVALID_ARG
