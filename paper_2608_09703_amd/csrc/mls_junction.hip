@@ -162,12 +162,15 @@ __global__ __launch_bounds__(kJBlock) void junction_bwd_kernel(JunctionArgs a) {
       }
     }
   }
-  float ev[CPL][8];
+  // the fresh block's gradient is loaded here too, so that it is in flight
+  // while the row reduction runs
+  float ev[CPL][8], gdv[CPL][8];
 #pragma unroll
   for (int c = 0; c < CPL; ++c) {
     const int64_t k = ((int64_t)c * TPR + j) * 8;
     if (live && k < df) {
       load8(e + k, ev[c]);
+      load8(gf + k, gdv[c]);
 #pragma unroll
       for (int i = 0; i < 8; ++i) s[1] = fmaf(ev[c][i], ev[c][i], s[1]);
     }
@@ -195,8 +198,8 @@ __global__ __launch_bounds__(kJBlock) void junction_bwd_kernel(JunctionArgs a) {
       store8(go + k, out);
     }
     if (k < df) {
-      float gd[8], out[8];
-      load8(gf + k, gd);
+      float out[8];
+      const float* gd = gdv[c];
       if (a.accumulate) load8(ge + k, out);
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
@@ -253,16 +256,22 @@ hipError_t bwd_tpr(const JunctionArgs& a, int tpr, int cpl, dim3 grid, hipStream
 }  // namespace
 
 // Threads per row and 8-element chunks per lane for rows of up to `width`
-// elements per operand: the fewest threads with at most 4 chunks each.
+// elements per operand: the fewest threads with at most 2 chunks each (more
+// memory-level parallelism per byte of registers), else 256 threads with 4.
 bool junction_shape(int64_t width, int* tpr, int* cpl) {
   const int64_t chunks = (width + 7) / 8;
   for (int t : {64, 128, 256})
-    for (int c : {1, 2, 4})
+    for (int c : {1, 2})
       if ((int64_t)t * c >= chunks) {
         *tpr = t;
         *cpl = c;
         return true;
       }
+  if (chunks <= (int64_t)kJBlock * 4) {
+    *tpr = kJBlock;
+    *cpl = 4;
+    return true;
+  }
   return false;
 }
 

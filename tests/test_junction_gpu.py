@@ -79,12 +79,14 @@ def _check(o, e, gx, layout, what, accumulate=False):
 
 SMALL = [
     # T, d_prev, d_fresh, act, grad, layout
-    (37, 8, 8, "bf16", "f32", "prev_first"),            # 64 threads, lane 0 only
+    # (threads per row x chunks per lane)
+    (37, 8, 8, "bf16", "f32", "prev_first"),            # 64 x 1, lane 0 only
     (300, 512, 256, "bf16", "bf16", "prev_first"),      # 64 x 1
     (301, 1024, 520, "bf16", "f32", "fresh_first"),     # 64 x 2, partial chunk
-    (129, 2048, 1024, "f32", "f32", "prev_first"),      # 64 x 4
-    (130, 3072, 1536, "bf16", "f32", "prev_first"),     # 128 x 4 (c5 junction 2)
+    (129, 2048, 1024, "f32", "f32", "prev_first"),      # 128 x 2
+    (130, 3072, 1536, "bf16", "f32", "prev_first"),     # 256 x 2 (c5 junction 2)
     (66, 4352, 2048, "f32", "bf16", "fresh_first"),     # 256 x 4
+    (67, 1544, 1032, "bf16", "bf16", "prev_first"),     # 128 x 2, ragged chunk coverage
     (5, 8192, 8, "bf16", "bf16", "prev_first"),         # widest row, tiny fresh block
     (1, 64, 8192, "f32", "f32", "fresh_first"),         # T = 1, widest fresh block
 ]
