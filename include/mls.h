@@ -237,6 +237,71 @@ mls_status mls_junction_bwd(const mls_junction* j, const void* o, const void* e,
                             void* g_o, void* g_e, void* stream);
 
 /*
+ * Head step of nested speculative decoding (paper section 2, paragraph
+ * "Speculative Decoding"; section 3 measures greedy and nucleus top-p 0.9
+ * sampling at temperature 0.4). A smaller sub-model drafts gamma tokens and a
+ * larger one verifies them; each step maps hidden states to logits with that
+ * sub-model's LM head and samples from them.
+ *
+ * Sampling distribution of a row of logits l: softmax(l / temperature), then
+ * the nucleus filter keeps the most probable tokens (ties: lower index first)
+ * up to and including the first one at which the kept mass reaches top_p, and
+ * renormalises (top_p = 1 keeps every token). Random numbers are inputs:
+ * uniforms in [0, 1). A draw with uniform u returns the smallest index whose
+ * cumulative kept probability, in index order, exceeds u. Greedy mode takes
+ * the argmax (lowest index on ties). Rows of up to 65536 entries.
+ */
+typedef struct mls_sampling {
+  int64_t V;          /* vocabulary size, 2..65536 */
+  float temperature;  /* > 0 (ignored when greedy) */
+  float top_p;        /* in (0, 1] (ignored when greedy) */
+  int32_t greedy;     /* nonzero: argmax */
+  int32_t reserved;   /* 0 */
+} mls_sampling;
+
+/*
+ * logits[t][v] = sum_k o[t][k] W[v][k] (fp32 row-major [T][V]) for o [T][d]
+ * and W [V][d] of dtype (MLS_BF16: d a multiple of 8; MLS_F32: of 4), all
+ * device arrays, 16-byte aligned. Asynchronous on stream.
+ */
+mls_status mls_head_logits(int64_t T, int64_t V, int64_t d, int32_t dtype, const void* o,
+                           const void* W, float* logits, void* stream);
+
+/*
+ * tokens[r] (int32, device) = a draw from row r of logits [rows][V] with
+ * uniform u[r] (device [rows]; may be NULL when greedy).
+ */
+mls_status mls_sample(const mls_sampling* s, int64_t rows, const float* logits, const float* u,
+                      int32_t* tokens, void* stream);
+
+/* Workspace bytes of mls_spec_verify for a batch and draft length. */
+mls_status mls_spec_verify_workspace(int64_t batch, int64_t gamma, size_t* bytes);
+
+/*
+ * Speculative verification of `batch` sequences with `gamma` >= 0 drafted
+ * tokens each (device arrays):
+ *   draft_logits  [batch][gamma][V]      the draft's logits at each drafted position
+ *   target_logits [batch][gamma + 1][V]  the verifier's logits at the same positions
+ *                                        and the one after them
+ *   draft_tokens  [batch][gamma] int32   the drafted tokens
+ *   u_accept      [batch][gamma]         uniforms of the acceptance tests
+ *   u_sample      [batch]                uniform of the final draw
+ * Per sequence, drafted token x at position k is kept when
+ * u_accept * q(x) < p(x) (q: the draft's sampling distribution, p: the
+ * verifier's). At the first rejection, next_token is drawn from max(0, p - q)
+ * renormalised and n_accepted = k; if all are kept, n_accepted = gamma and
+ * next_token is drawn from the verifier's distribution at position gamma.
+ * Greedy mode keeps a token while it equals the verifier's argmax and emits
+ * the verifier's argmax (u_accept, u_sample and the workspace may be NULL).
+ * Outputs n_accepted, next_token: int32 [batch]. Asynchronous on stream.
+ */
+mls_status mls_spec_verify(const mls_sampling* s, int64_t batch, int64_t gamma,
+                           const float* draft_logits, const float* target_logits,
+                           const int32_t* draft_tokens, const float* u_accept,
+                           const float* u_sample, int32_t* n_accepted, int32_t* next_token,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Host helper: loss coefficients of the objective (host arrays of length M).
  *   mode MLS_MODE_PAPER (eq. (3) summed over sub-models):
  *     student g_ce = w (1 - alpha), g_kl = w alpha tau^2; teacher g_ce = w, g_kl = 0

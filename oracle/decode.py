@@ -35,6 +35,9 @@ Readings taken where the paper does not fix the details (listed in the design doc):
   p(x)/q(x)`` without a division, and it keeps tokens the draft could not have
   produced (``q(x) = 0 < p(x)``) and never keeps tokens the verifier excludes.
 * Greedy argmax ties go to the lowest index.
+* After a rejection, ``max(0, p - q)`` has no mass only if the rejected token
+  is impossible under both distributions and the two coincide; the next token
+  is then drawn from ``p``.
 """
 
 from __future__ import annotations
@@ -111,7 +114,8 @@ def verify(draft_logits, target_logits, draft_tokens, u_accept, u_sample, temper
                 p = filtered_probs(target_logits[b][k], temperature, top_p)
                 q = filtered_probs(draft_logits[b][k], temperature, top_p)
                 if not (u_accept[b][k] * q[x] < p[x]):
-                    nxt[b] = draw(np.maximum(p - q, 0.0), u_sample[b])
+                    res = np.maximum(p - q, 0.0)
+                    nxt[b] = draw(res if res.sum() > 0 else p, u_sample[b])
                     break
             k += 1
         n_acc[b] = k

@@ -242,6 +242,69 @@ def junction(o: torch.Tensor, e: torch.Tensor, *, layout: str = "prev_first") ->
     return _Junction.apply(o, e, layout)
 
 
+def head_logits(o: torch.Tensor, W: torch.Tensor, out: Optional[torch.Tensor] = None):
+    """``logits [T, V] = o W^T`` in fp32 through the HIP head kernel (decode regime)."""
+    if o.device.type != "cuda" or W.device != o.device or o.dtype != W.dtype:
+        raise RuntimeError("o and W must be GPU tensors of one dtype")
+    if not (o.is_contiguous() and W.is_contiguous()) or o.shape[1] != W.shape[1]:
+        raise ValueError("o [T, d] and W [V, d] must be contiguous with a shared d")
+    T, V = o.shape[0], W.shape[0]
+    out = out if out is not None else torch.empty(T, V, dtype=torch.float32, device=o.device)
+    B.head_logits(T, V, o.shape[1], _dtype_code(o.dtype), o.data_ptr(), W.data_ptr(),
+                  out.data_ptr(), _stream(o.device))
+    return out
+
+
+def _sampling(V, temperature, top_p, greedy):
+    return B.make_sampling(V, temperature, top_p, greedy)
+
+
+def sample(logits: torch.Tensor, u: Optional[torch.Tensor], *, temperature: float = 1.0,
+           top_p: float = 1.0, greedy: bool = False) -> torch.Tensor:
+    """int32 tokens, one per row of ``logits [rows, V]`` (fp32), with uniforms ``u [rows]``."""
+    if logits.dtype != torch.float32 or not logits.is_contiguous() or logits.dim() != 2:
+        raise ValueError("logits must be a contiguous float32 [rows, V] tensor")
+    rows, V = logits.shape
+    if u is not None and (u.dtype != torch.float32 or u.shape != (rows,) or not u.is_contiguous()):
+        raise ValueError("u must be a contiguous float32 [rows] tensor")
+    tok = torch.empty(rows, dtype=torch.int32, device=logits.device)
+    B.sample(_sampling(V, temperature, top_p, greedy), rows, logits.data_ptr(),
+             u.data_ptr() if u is not None else None, tok.data_ptr(), _stream(logits.device))
+    return tok
+
+
+def spec_verify(draft_logits: Optional[torch.Tensor], target_logits: torch.Tensor,
+                draft_tokens: Optional[torch.Tensor], u_accept: Optional[torch.Tensor],
+                u_sample: Optional[torch.Tensor], *, temperature: float = 1.0, top_p: float = 1.0,
+                greedy: bool = False):
+    """``(n_accepted [B], next_token [B])`` (int32) of speculative verification.
+
+    ``draft_logits [B, gamma, V]``, ``target_logits [B, gamma + 1, V]`` (fp32),
+    ``draft_tokens [B, gamma]`` (int32), ``u_accept [B, gamma]``, ``u_sample [B]``.
+    """
+    Bt, G1, V = target_logits.shape
+    G = G1 - 1
+    dev = target_logits.device
+    for x in (draft_logits, target_logits, u_accept, u_sample):
+        if x is not None and (x.dtype != torch.float32 or not x.is_contiguous()):
+            raise ValueError("logits and uniforms must be contiguous float32")
+    if draft_tokens is not None and (draft_tokens.dtype != torch.int32 or
+                                     not draft_tokens.is_contiguous()):
+        raise ValueError("draft_tokens must be contiguous int32")
+    if G > 0 and (draft_logits is None or draft_logits.shape != (Bt, G, V) or
+                  draft_tokens is None or draft_tokens.shape != (Bt, G)):
+        raise ValueError("draft_logits [B, gamma, V] and draft_tokens [B, gamma] are required")
+    n_acc = torch.empty(Bt, dtype=torch.int32, device=dev)
+    nxt = torch.empty(Bt, dtype=torch.int32, device=dev)
+    ws_bytes = 0 if greedy else B.spec_verify_workspace(Bt, G)
+    ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev) if not greedy else None
+    ptr = (lambda x: x.data_ptr() if x is not None else None)
+    B.spec_verify(_sampling(V, temperature, top_p, greedy), Bt, G, ptr(draft_logits),
+                  target_logits.data_ptr(), ptr(draft_tokens), ptr(u_accept), ptr(u_sample),
+                  n_acc.data_ptr(), nxt.data_ptr(), ptr(ws), ws_bytes, _stream(dev))
+    return n_acc, nxt
+
+
 def coefficients(M: int, *, alpha: float, tau: float = 1.0, teacher: int = -1,
                  mode: str = "paper", weights: Optional[Sequence[float]] = None):
     """``(g_ce, g_kl)`` lists of eq. (3) (``mode="paper"``) or the additive form."""

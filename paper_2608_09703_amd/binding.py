@@ -45,6 +45,10 @@ EXPORTED = (
     "mls_diagnostics",
     "mls_junction_fwd",
     "mls_junction_bwd",
+    "mls_head_logits",
+    "mls_sample",
+    "mls_spec_verify_workspace",
+    "mls_spec_verify",
     "mls_coeffs",
     "mls_read_stats_header",
     "mls_status_string",
@@ -85,6 +89,16 @@ class Problem(ctypes.Structure):
     ]
 
 
+class Sampling(ctypes.Structure):
+    _fields_ = [
+        ("V", ctypes.c_int64),
+        ("temperature", ctypes.c_float),
+        ("top_p", ctypes.c_float),
+        ("greedy", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+    ]
+
+
 class Junction(ctypes.Structure):
     _fields_ = [
         ("T", ctypes.c_int64),
@@ -119,6 +133,14 @@ def lib():
         J = ctypes.POINTER(Junction)
         L.mls_junction_fwd.argtypes = [J, vp, vp, vp, vp]
         L.mls_junction_bwd.argtypes = [J, vp, vp, vp, vp, vp, vp]
+        S = ctypes.POINTER(Sampling)
+        L.mls_head_logits.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                      vp, vp, vp, vp]
+        L.mls_sample.argtypes = [S, ctypes.c_int64, vp, vp, vp, vp]
+        L.mls_spec_verify_workspace.argtypes = [ctypes.c_int64, ctypes.c_int64,
+                                                ctypes.POINTER(ctypes.c_size_t)]
+        L.mls_spec_verify.argtypes = [S, ctypes.c_int64, ctypes.c_int64, vp, vp, vp, vp, vp, vp, vp,
+                                      vp, ctypes.c_size_t, vp]
         L.mls_coeffs.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_float, ctypes.c_float,
                                  ctypes.c_int32, fp, fp, fp]
         L.mls_read_stats_header.argtypes = [P, vp, vp, ctypes.POINTER(ctypes.c_int32),
@@ -213,6 +235,36 @@ def junction_fwd(j: Junction, o: int, e: int, x: int, stream: int):
 
 def junction_bwd(j: Junction, o: int, e: int, g_x: int, g_o: int, g_e: int, stream: int):
     check(lib().mls_junction_bwd(ctypes.byref(j), o, e, g_x, g_o, g_e, stream), "mls_junction_bwd")
+
+
+def make_sampling(V: int, temperature: float = 1.0, top_p: float = 1.0,
+                  greedy: bool = False) -> Sampling:
+    s = Sampling()
+    s.V, s.temperature, s.top_p, s.greedy, s.reserved = V, temperature, top_p, int(bool(greedy)), 0
+    return s
+
+
+def head_logits(T: int, V: int, d: int, dtype: int, o: int, W: int, logits: int, stream: int):
+    check(lib().mls_head_logits(T, V, d, dtype, o, W, logits, stream), "mls_head_logits")
+
+
+def sample(s: Sampling, rows: int, logits: int, u: Optional[int], tokens: int, stream: int):
+    check(lib().mls_sample(ctypes.byref(s), rows, logits, u, tokens, stream), "mls_sample")
+
+
+def spec_verify_workspace(batch: int, gamma: int) -> int:
+    n = ctypes.c_size_t(0)
+    check(lib().mls_spec_verify_workspace(batch, gamma, ctypes.byref(n)), "mls_spec_verify_workspace")
+    return n.value
+
+
+def spec_verify(s: Sampling, batch: int, gamma: int, draft_logits: Optional[int],
+                target_logits: int, draft_tokens: Optional[int], u_accept: Optional[int],
+                u_sample: Optional[int], n_accepted: int, next_token: int, ws: Optional[int],
+                ws_bytes: int, stream: int):
+    check(lib().mls_spec_verify(ctypes.byref(s), batch, gamma, draft_logits, target_logits,
+                                draft_tokens, u_accept, u_sample, n_accepted, next_token, ws,
+                                ws_bytes, stream), "mls_spec_verify")
 
 
 def coeffs(M: int, teacher: int = -1, alpha: float = 0.0, tau: float = 1.0,

@@ -727,6 +727,168 @@ mls_status mls_junction_bwd(const mls_junction* j, const void* o, const void* e,
   return MLS_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+mls_status validate_sampling(const mls_sampling* s) {
+  if (!s) return fail(MLS_INVALID_ARG, "sampling descriptor is NULL");
+  if (s->V < 2 || s->V > 65536) return fail(MLS_UNSUPPORTED, "V=%lld outside [2, 65536]", (long long)s->V);
+  if (!s->greedy) {
+    if (!(s->temperature > 0.f) || !isfinite(s->temperature))
+      return fail(MLS_INVALID_ARG, "temperature must be finite and > 0");
+    if (!(s->top_p > 0.f) || s->top_p > 1.f) return fail(MLS_INVALID_ARG, "top_p must be in (0, 1]");
+  }
+  if (s->reserved != 0) return fail(MLS_INVALID_ARG, "reserved field must be 0");
+  return MLS_OK;
+}
+
+size_t verify_ws_bytes(int64_t batch, int64_t gamma) {
+  return align256((size_t)(batch * gamma + batch * (gamma + 1)) * sizeof(RowDist));
+}
+
+}  // namespace
+
+extern "C" {
+
+mls_status mls_head_logits(int64_t T, int64_t V, int64_t d, int32_t dtype, const void* o,
+                           const void* W, float* logits, void* stream) {
+  g_last_error.clear();
+  if (T < 1 || T > (1ll << 30) || V < 1 || V > (1ll << 30) || d < 1 || d > (1 << 20))
+    return fail(MLS_INVALID_ARG, "T=%lld V=%lld d=%lld out of range", (long long)T, (long long)V,
+                (long long)d);
+  if (dtype != MLS_BF16 && dtype != MLS_F32) return fail(MLS_UNSUPPORTED, "dtype=%d unsupported", dtype);
+  if (d % (dtype == MLS_BF16 ? 8 : 4))
+    return fail(MLS_UNSUPPORTED, "d=%lld is not a multiple of %d", (long long)d,
+                dtype == MLS_BF16 ? 8 : 4);
+  if (!o || !W || !logits) return fail(MLS_INVALID_ARG, "o, W and logits must be non-NULL");
+  if (!aligned(o, 16) || !aligned(W, 16) || !aligned(logits, 16))
+    return fail(MLS_INVALID_ARG, "o, W and logits must be 16-byte aligned");
+  HeadArgs a;
+  memset(&a, 0, sizeof(a));
+  a.T = T;
+  a.V = V;
+  a.d = d;
+  a.o = o;
+  a.W = W;
+  a.logits = logits;
+  a.n_tt = (int)((T + head_tile() - 1) / head_tile());
+  a.n_vt = (int)((V + head_tile() - 1) / head_tile());
+  a.group_v = 8;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  {
+    ProfScope ps("head_logits", st);
+    e = launch_head_logits(a, dtype == MLS_F32, dtype == MLS_BF16 && d % 64 == 0, st);
+  }
+  if (e != hipSuccess) return hip_fail(e, "head logits launch");
+  return MLS_OK;
+}
+
+mls_status mls_sample(const mls_sampling* s, int64_t rows, const float* logits, const float* u,
+                      int32_t* tokens, void* stream) {
+  g_last_error.clear();
+  mls_status st = validate_sampling(s);
+  if (st != MLS_OK) return st;
+  if (rows < 1 || rows > (1ll << 31) - 1) return fail(MLS_INVALID_ARG, "rows=%lld out of range", (long long)rows);
+  if (!logits || !tokens || (!s->greedy && !u))
+    return fail(MLS_INVALID_ARG, "logits, tokens and (unless greedy) u must be non-NULL");
+  if (!aligned(logits, 4) || !aligned(u, 4) || !aligned(tokens, 4))
+    return fail(MLS_INVALID_ARG, "misaligned pointer");
+  SampleArgs a;
+  memset(&a, 0, sizeof(a));
+  a.rows = rows;
+  a.V = s->V;
+  a.inv_temp = s->greedy ? 1.f : 1.f / s->temperature;
+  a.top_p = s->top_p;
+  a.greedy = s->greedy ? 1 : 0;
+  a.logits = logits;
+  a.u = u;
+  a.tokens = tokens;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  {
+    ProfScope ps("sample", hs);
+    e = launch_sample(a, row_elems_per_thread(s->V), hs);
+  }
+  if (e != hipSuccess) return hip_fail(e, "sample launch");
+  return MLS_OK;
+}
+
+mls_status mls_spec_verify_workspace(int64_t batch, int64_t gamma, size_t* bytes) {
+  g_last_error.clear();
+  if (batch < 1 || gamma < 0 || batch > (1 << 24) || gamma > 1024)
+    return fail(MLS_INVALID_ARG, "batch=%lld gamma=%lld out of range", (long long)batch, (long long)gamma);
+  if (!bytes) return fail(MLS_INVALID_ARG, "bytes is NULL");
+  *bytes = verify_ws_bytes(batch, gamma);
+  return MLS_OK;
+}
+
+mls_status mls_spec_verify(const mls_sampling* s, int64_t batch, int64_t gamma,
+                           const float* draft_logits, const float* target_logits,
+                           const int32_t* draft_tokens, const float* u_accept,
+                           const float* u_sample, int32_t* n_accepted, int32_t* next_token,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  mls_status st = validate_sampling(s);
+  if (st != MLS_OK) return st;
+  if (batch < 1 || gamma < 0 || batch > (1 << 24) || gamma > 1024)
+    return fail(MLS_INVALID_ARG, "batch=%lld gamma=%lld out of range", (long long)batch, (long long)gamma);
+  if (!target_logits || !n_accepted || !next_token || (gamma > 0 && (!draft_logits || !draft_tokens)))
+    return fail(MLS_INVALID_ARG, "logits, draft tokens and outputs must be non-NULL");
+  if (!s->greedy && (!u_sample || (gamma > 0 && !u_accept)))
+    return fail(MLS_INVALID_ARG, "sampling needs u_accept and u_sample");
+  if (!s->greedy && !workspace) return fail(MLS_INVALID_ARG, "sampling needs the workspace");
+  if (!s->greedy && workspace_bytes < verify_ws_bytes(batch, gamma))
+    return fail(MLS_WORKSPACE_TOO_SMALL, "verification needs %zu workspace bytes, got %zu",
+                verify_ws_bytes(batch, gamma), workspace_bytes);
+  if (!aligned(workspace, 16)) return fail(MLS_INVALID_ARG, "misaligned workspace");
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  const int ept = row_elems_per_thread(s->V);
+  const float inv_temp = s->greedy ? 1.f : 1.f / s->temperature;
+  hipError_t e;
+  RowDist* params = static_cast<RowDist*>(workspace);
+  if (!s->greedy) {
+    RowParamArgs r;
+    memset(&r, 0, sizeof(r));
+    r.rows0 = batch * gamma;
+    r.rows1 = batch * (gamma + 1);
+    r.V = s->V;
+    r.inv_temp = inv_temp;
+    r.top_p = s->top_p;
+    r.logits0 = draft_logits;
+    r.logits1 = target_logits;
+    r.params = params;
+    {
+      ProfScope ps("row_params", hs);
+      e = launch_row_params(r, ept, hs);
+    }
+    if (e != hipSuccess) return hip_fail(e, "row parameter launch");
+  }
+  VerifyArgs a;
+  memset(&a, 0, sizeof(a));
+  a.params = params;
+  a.batch = batch;
+  a.V = s->V;
+  a.gamma = (int32_t)gamma;
+  a.greedy = s->greedy ? 1 : 0;
+  a.inv_temp = inv_temp;
+  a.top_p = s->top_p;
+  a.draft_logits = draft_logits;
+  a.target_logits = target_logits;
+  a.draft_tokens = draft_tokens;
+  a.u_accept = u_accept;
+  a.u_sample = u_sample;
+  a.n_accepted = n_accepted;
+  a.next_token = next_token;
+  {
+    ProfScope ps("spec_verify", hs);
+    e = launch_verify(a, ept, hs);
+  }
+  if (e != hipSuccess) return hip_fail(e, "verification launch");
+  return MLS_OK;
+}
+
 mls_status mls_read_stats_header(const mls_problem* p, const void* stats, void* stream,
                                  int32_t* n_valid, int32_t* device_flags) {
   g_last_error.clear();

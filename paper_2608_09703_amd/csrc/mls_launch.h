@@ -172,6 +172,63 @@ struct JunctionArgs {
   void* g_e;        // [T][d_fresh]
 };
 
+// Speculative-decoding head step.
+struct HeadArgs {
+  int64_t T;       // rows (tokens)
+  int64_t V;
+  int64_t d;
+  const void* o;   // [T][d]
+  const void* W;   // [V][d]
+  float* logits;   // [T][V]
+  int32_t n_tt;
+  int32_t n_vt;
+  int32_t group_v;
+};
+struct SampleArgs {
+  int64_t rows;
+  int64_t V;
+  float inv_temp;
+  float top_p;
+  int32_t greedy;
+  const float* logits;  // [rows][V]
+  const float* u;       // [rows]
+  int32_t* tokens;      // [rows]
+};
+// Parameters of one row's sampling distribution.
+struct RowDist {
+  float m;      // max logit / temperature
+  float total;  // sum of exp weights exp(l / temperature - m)
+  float theta;  // nucleus threshold on the exp weight (0: keep every positive weight)
+  int tie_cut;  // tokens with weight == theta are kept for index <= tie_cut
+  float kept;   // sum of kept weights
+};
+struct RowParamArgs {
+  int64_t rows0;          // rows of logits0, then rows1 rows of logits1
+  int64_t rows1;
+  int64_t V;
+  float inv_temp;
+  float top_p;
+  const float* logits0;
+  const float* logits1;
+  RowDist* params;        // [rows0 + rows1]
+};
+struct VerifyArgs {
+  const RowDist* params;  // draft rows [batch][gamma], then verifier rows [batch][gamma + 1]
+  int64_t batch;
+  int64_t V;
+  int32_t gamma;
+  int32_t greedy;
+  float inv_temp;
+  float top_p;
+  const float* draft_logits;   // [batch][gamma][V]
+  const float* target_logits;  // [batch][gamma + 1][V]
+  const int32_t* draft_tokens; // [batch][gamma]
+  const float* u_accept;       // [batch][gamma]
+  const float* u_sample;       // [batch]
+  int32_t* n_accepted;         // [batch]
+  int32_t* next_token;         // [batch]
+};
+
 // Launchers (each enqueues on `stream` and returns the launch status).
 int fused_tile_rows(bool wide);
 hipError_t launch_fused_fwd(const FusedArgs& a, bool f32, hipStream_t stream);
@@ -193,6 +250,12 @@ bool junction_shape(int64_t width, int* tpr, int* cpl);
 int64_t junction_max_width();
 hipError_t launch_junction_fwd(const JunctionArgs& a, bool act_f32, hipStream_t stream);
 hipError_t launch_junction_bwd(const JunctionArgs& a, bool act_f32, bool grad_f32, hipStream_t stream);
+int head_tile();
+int row_elems_per_thread(int64_t V);
+hipError_t launch_head_logits(const HeadArgs& a, bool f32, bool wide, hipStream_t stream);
+hipError_t launch_sample(const SampleArgs& a, int ept, hipStream_t stream);
+hipError_t launch_row_params(const RowParamArgs& a, int ept, hipStream_t stream);
+hipError_t launch_verify(const VerifyArgs& a, int ept, hipStream_t stream);
 hipError_t launch_label_logits(const RowArgs& a, bool f32, hipStream_t stream);
 hipError_t launch_finalize_rows(const RowArgs& a, hipStream_t stream);
 hipError_t launch_reduce_losses(const RowArgs& a, hipStream_t stream);

@@ -166,3 +166,65 @@ def make_junction_inputs(wl: JunctionWorkload, m: int, device="cpu", seed: Optio
     gx = (torch.randn(T, d_prev + d_fresh, generator=g, device=device) * wl.g_std).to(
         _dt(wl.grad_dtype))
     return o, e, gx
+
+
+# ---------------------------------------------------------------------------
+# speculative-decoding head step inputs
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class DecodeWorkload:
+    """One decoding step of a draft / verifier pair (section 3, "Speculative
+    Decoding Throughput": a 500M draft and the 3B verifier, batches of up to 102
+    sequences, draft length gamma, nucleus 0.9 at temperature 0.4).
+
+    The draft's head and hidden states are the leading ``d_draft`` columns of
+    the verifier's (nested sub-models share their leading parameters), so the
+    two distributions are related as a draft and its verifier are. Hidden states
+    are N(0, o_std^2), heads N(0, w_std^2); with these values the temperature-0.4
+    distributions are peaked (nuclei of a few to a few hundred tokens).
+    """
+
+    name: str
+    batch: int
+    gamma: int
+    V: int
+    d_draft: int
+    d_target: int
+    temperature: float = 0.4
+    top_p: float = 0.9
+    o_std: float = 4.0
+    w_std: float = 0.02
+    seed: int = 0
+
+
+DECODE = {
+    "spec_500m_3b": DecodeWorkload("spec_500m_3b", 102, 6, 49152, 1024, 4352, seed=3001),
+    "spec_vanilla_b64": DecodeWorkload("spec_vanilla_b64", 64, 6, 49152, 1024, 4352, seed=3002),
+}
+
+
+def make_decode_inputs(wl: DecodeWorkload, device="cpu", seed: Optional[int] = None):
+    """Dict of bf16 heads / hidden states and fp32 uniforms for one step.
+
+    Draw order from one generator: W_target, o_target (rows [batch * (gamma + 1)],
+    sequence-major), the draft's hidden-state noise (rows [gamma * batch],
+    step-major), uniforms of the draft draws [gamma, batch], of the acceptance
+    tests [batch, gamma] and of the final draws [batch]. The draft's hidden
+    state at (step k, sequence b) is the leading d_draft columns of the
+    verifier's at the same position plus N(0, (o_std / 2)^2) noise.
+    """
+    g = torch.Generator(device=device)
+    g.manual_seed(wl.seed if seed is None else seed)
+    B, G = wl.batch, wl.gamma
+    Wt = (torch.randn(wl.V, wl.d_target, generator=g, device=device) * wl.w_std).to(torch.bfloat16)
+    ot = (torch.randn(B * (G + 1), wl.d_target, generator=g, device=device) * wl.o_std).to(
+        torch.bfloat16)
+    noise = torch.randn(G * B, wl.d_draft, generator=g, device=device) * (wl.o_std / 2)
+    pos = (torch.arange(B, device=device)[None, :] * (G + 1) + torch.arange(G, device=device)[:, None])
+    od = (ot[pos.reshape(-1), :wl.d_draft].float() + noise).to(torch.bfloat16)
+    u_draft = torch.rand(G, B, generator=g, device=device)
+    u_accept = torch.rand(B, G, generator=g, device=device)
+    u_sample = torch.rand(B, generator=g, device=device)
+    return {"W_target": Wt, "W_draft": Wt[:, :wl.d_draft].contiguous(), "o_target": ot,
+            "o_draft": od, "u_draft": u_draft, "u_accept": u_accept, "u_sample": u_sample}

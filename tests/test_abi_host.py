@@ -39,7 +39,8 @@ def test_version_and_status_strings():
     assert L.mls_status_string(B.MLS_WORKSPACE_TOO_SMALL) == b"workspace too small"
 
 
-@pytest.mark.parametrize("cname,cls", [("mls_problem", B.Problem), ("mls_junction", B.Junction)])
+@pytest.mark.parametrize("cname,cls", [("mls_problem", B.Problem), ("mls_junction", B.Junction),
+                                       ("mls_sampling", B.Sampling)])
 def test_struct_layout_matches_header(tmp_path, cname, cls):
     """The ctypes mirrors of the C structs have the C compiler's layout."""
     import shutil
@@ -224,4 +225,55 @@ def test_junction_rejects_bad_pointers_before_device_work():
     assert e.value.status == B.MLS_INVALID_ARG
     with pytest.raises(B.MlsError) as e:
         B.junction_bwd(j, fake, None, fake + (2 << 30), fake + (3 << 30), fake + (4 << 30), None)
+    assert e.value.status == B.MLS_INVALID_ARG
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("V", 1, B.MLS_UNSUPPORTED),
+    ("V", 65537, B.MLS_UNSUPPORTED),
+    ("temperature", 0.0, B.MLS_INVALID_ARG),
+    ("temperature", math.inf, B.MLS_INVALID_ARG),
+    ("top_p", 0.0, B.MLS_INVALID_ARG),
+    ("top_p", 1.5, B.MLS_INVALID_ARG),
+    ("reserved", 1, B.MLS_INVALID_ARG),
+])
+def test_sampling_rejects_bad_descriptors_before_device_work(field, value, status):
+    s = B.make_sampling(49152, 0.4, 0.9)
+    setattr(s, field, value)
+    fake = 1 << 40
+    with pytest.raises(B.MlsError) as e:
+        B.sample(s, 102, fake, fake + (1 << 30), fake + (2 << 30), None)
+    assert e.value.status == status
+    ws = B.spec_verify_workspace(102, 6)
+    with pytest.raises(B.MlsError) as e:
+        B.spec_verify(s, 102, 6, fake, fake + (1 << 32), fake + (2 << 32), fake + (3 << 32),
+                      fake + (4 << 32), fake + (5 << 32), fake + (6 << 32), fake + (7 << 32), ws,
+                      None)
+    assert e.value.status == status
+
+
+def test_decode_entry_points_reject_bad_arguments_before_device_work():
+    fake = 1 << 40
+    s = B.make_sampling(49152, 0.4, 0.9)
+    with pytest.raises(B.MlsError) as e:  # sampling without uniforms
+        B.sample(s, 4, fake, None, fake + 4096, None)
+    assert e.value.status == B.MLS_INVALID_ARG
+    ws = B.spec_verify_workspace(8, 6)
+    assert ws >= (8 * 6 + 8 * 7) * 20
+    with pytest.raises(B.MlsError) as e:
+        B.spec_verify(s, 8, 6, fake, fake + (1 << 32), fake + (2 << 32), fake + (3 << 32),
+                      fake + (4 << 32), fake + (5 << 32), fake + (6 << 32), fake + (7 << 32), 64,
+                      None)
+    assert e.value.status == B.MLS_WORKSPACE_TOO_SMALL
+    with pytest.raises(B.MlsError) as e:  # drafts without their logits
+        B.spec_verify(s, 8, 6, None, fake + (1 << 32), fake + (2 << 32), fake + (3 << 32),
+                      fake + (4 << 32), fake + (5 << 32), fake + (6 << 32), fake + (7 << 32), ws,
+                      None)
+    assert e.value.status == B.MLS_INVALID_ARG
+    with pytest.raises(B.MlsError) as e:
+        B.head_logits(102, 49152, 1030, B.MLS_BF16, fake, fake + (1 << 32), fake + (2 << 32), None)
+    assert e.value.status == B.MLS_UNSUPPORTED
+    with pytest.raises(B.MlsError) as e:
+        B.head_logits(102, 49152, 1024, B.MLS_BF16, fake + 8, fake + (1 << 32), fake + (2 << 32),
+                      None)
     assert e.value.status == B.MLS_INVALID_ARG

@@ -1,0 +1,319 @@
+"""GPU parity of the speculative-decoding head step against the float64 oracle.
+
+* Head logits: fp32 accumulation of d bf16 products; per element the error is
+  bounded by 1e-5 of sum_k |o_k W_vk| (well above fp32 rounding of d <= 8192
+  terms) plus 1e-6.
+* Sampling and verification take integer decisions (nucleus membership, the
+  inverse-CDF position, acceptance) from fp32 arithmetic on the GPU and fp64 in
+  the oracle, on the same fp32 logits. A GPU result that differs from the
+  oracle's is accepted only when the oracle reproduces it under a perturbation
+  of 1e-5 of its inputs (the uniform, top_p, or the acceptance ratio), and such
+  rows must stay rare. Greedy decisions are taken on identical fp32 values and
+  must match exactly.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import decode as OD
+from paper_2608_09703_amd import api as D
+from paper_2608_09703_amd import workloads as WL
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+EPS = 1e-5
+
+
+def _np(x):
+    return x.detach().cpu().numpy()
+
+
+# ---------------------------------------------------------------------------
+# head logits
+# ---------------------------------------------------------------------------
+
+HEAD = [
+    # T, V, d, dtype
+    (102, 1000, 1024, torch.bfloat16),   # wide bf16 core, one token tile
+    (714, 777, 4352, torch.bfloat16),    # ragged V (scalar stores), several token tiles
+    (5, 49152, 1024, torch.bfloat16),    # full vocabulary, tiny batch
+    (130, 513, 1000, torch.bfloat16),    # general bf16 core (d not a multiple of 64)
+    (33, 300, 100, torch.float32),       # fp32 core
+]
+
+
+@pytest.mark.parametrize("case", HEAD, ids=[f"T{c[0]}_V{c[1]}_d{c[2]}_{str(c[3])[6:]}" for c in HEAD])
+def test_head_logits(case):
+    T, V, d, dt = case
+    print(f"[decode] head logits T={T} V={V} d={d} {dt}", flush=True)
+    g = torch.Generator(device=DEV).manual_seed(T + V + d)
+    o = (torch.randn(T, d, generator=g, device=DEV) * 4).to(dt)
+    W = (torch.randn(V, d, generator=g, device=DEV) * 0.02).to(dt)
+    got = _np(D.head_logits(o, W)).astype(np.float64)
+    on, Wn = _np(o.float()).astype(np.float64), _np(W.float()).astype(np.float64)
+    ref = OD.head_logits(on, Wn)
+    bound = 1e-5 * (np.abs(on) @ np.abs(Wn).T) + 1e-6
+    bad = np.abs(got - ref) > bound
+    assert not bad.any(), f"{bad.sum()} logits off, first {np.argwhere(bad)[0]}"
+
+
+# ---------------------------------------------------------------------------
+# sampling
+# ---------------------------------------------------------------------------
+
+def _oracle_tokens_near(row, u, temperature, top_p):
+    """Tokens the oracle draws under perturbations of u and top_p by EPS."""
+    out = set()
+    for du in (-EPS, 0.0, EPS):
+        for dp in (-EPS, 0.0, EPS):
+            uu = min(max(u + du, 0.0), 1.0 - 1e-12)
+            pp = min(max(top_p + dp, 1e-9), 1.0)
+            out.add(int(OD.draw(OD.filtered_probs(row, temperature, pp), uu)))
+    return out
+
+
+def _check_samples(logits, u, tokens, temperature, top_p, max_ambiguous=0.02):
+    ref = OD.sample(logits, u, temperature, top_p)
+    miss = np.nonzero(ref != tokens)[0]
+    for r in miss:
+        near = _oracle_tokens_near(logits[r], float(u[r]), temperature, top_p)
+        assert int(tokens[r]) in near, (f"row {r}: GPU token {tokens[r]}, oracle {ref[r]}, "
+                                        f"oracle under perturbation {sorted(near)}")
+    assert len(miss) <= max(1, max_ambiguous * len(tokens)), f"{len(miss)} ambiguous rows"
+    return len(miss)
+
+
+SAMPLE = [
+    # rows, V, temperature, top_p, logit scale
+    (64, 1000, 0.4, 0.9, 3.0),
+    (33, 3000, 1.0, 1.0, 1.0),     # plain softmax, ragged V (not a multiple of 1024)
+    (40, 49152, 0.4, 0.9, 2.5),    # paper vocabulary
+    (17, 20000, 0.7, 0.5, 1.5),
+    (12, 2, 1.0, 0.9, 1.0),        # V = 2
+    (9, 5000, 0.4, 1e-7, 2.0),     # tiny top_p: the argmax
+    (8, 60000, 0.4, 0.95, 2.0),    # 64 values per thread
+]
+
+
+@pytest.mark.parametrize("case", SAMPLE, ids=[f"r{c[0]}_V{c[1]}_t{c[2]}_p{c[3]}" for c in SAMPLE])
+def test_sample_parity(case):
+    rows, V, temp, top_p, scale = case
+    print(f"[decode] sample rows={rows} V={V} T={temp} p={top_p}", flush=True)
+    g = torch.Generator(device=DEV).manual_seed(rows * 7 + V)
+    logits = torch.randn(rows, V, generator=g, device=DEV) * scale
+    u = torch.rand(rows, generator=g, device=DEV)
+    tok = _np(D.sample(logits, u, temperature=temp, top_p=top_p)).astype(np.int64)
+    _check_samples(_np(logits).astype(np.float64), _np(u).astype(np.float64), tok, temp, top_p)
+    greedy = _np(D.sample(logits, None, greedy=True)).astype(np.int64)
+    assert np.array_equal(greedy, _np(logits).argmax(axis=1))
+
+
+def test_sample_ties_and_extreme_uniforms():
+    """Exactly tied logits straddling the nucleus boundary (lower indices kept
+    first), and uniforms at 0 and just below 1."""
+    V = 4096
+    row = np.full(V, -30.0, dtype=np.float32)
+    row[[5, 900, 1500, 3000, 4000]] = 2.0  # five tied leaders
+    row[2000] = 1.0
+    logits = torch.tensor(np.tile(row, (6, 1)), device=DEV)
+    u = torch.tensor([0.0, 0.2, 0.5, 0.7, 0.9999999, 0.999], device=DEV)
+    for top_p in (0.3, 0.5, 0.95, 1.0):
+        tok = _np(D.sample(logits, u, temperature=1.0, top_p=top_p)).astype(np.int64)
+        ref = OD.sample(_np(logits).astype(np.float64), _np(u).astype(np.float64), 1.0, top_p)
+        assert np.array_equal(tok, ref), (top_p, tok, ref)
+    greedy = _np(D.sample(logits, None, greedy=True))
+    assert np.all(greedy == 5)
+
+
+def test_sample_frequencies_on_a_uniform_grid():
+    """A row drawn with a grid of uniforms reproduces the oracle's distribution."""
+    V, N = 2500, 4096
+    g = torch.Generator(device=DEV).manual_seed(11)
+    row = torch.randn(V, generator=g, device=DEV) * 2.0
+    logits = row[None, :].repeat(N, 1).contiguous()
+    u = (torch.arange(N, device=DEV, dtype=torch.float32) + 0.5) / N
+    tok = _np(D.sample(logits, u, temperature=0.4, top_p=0.9)).astype(np.int64)
+    p = OD.filtered_probs(_np(row).astype(np.float64), 0.4, 0.9)
+    freq = np.bincount(tok, minlength=V) / N
+    np.testing.assert_allclose(freq, p, atol=2.0 / N)
+    assert freq[p == 0].sum() == 0
+
+
+# ---------------------------------------------------------------------------
+# verification
+# ---------------------------------------------------------------------------
+
+def _ambiguous_sequence(dl, tl, drafts, ua, us, temp, top_p, b):
+    """Whether the oracle's result for sequence b changes under perturbations."""
+    base = OD.verify(dl[b:b + 1], tl[b:b + 1], drafts[b:b + 1], ua[b:b + 1], us[b:b + 1], temp,
+                     top_p)
+    outs = set()
+    for da in (-EPS, 0.0, EPS):
+        for ds in (-EPS, 0.0, EPS):
+            for dp in (-EPS, 0.0, EPS):
+                n, x = OD.verify(dl[b:b + 1], tl[b:b + 1], drafts[b:b + 1],
+                                 np.clip(ua[b:b + 1] * (1 + da), 0, 1 - 1e-12),
+                                 np.clip(us[b:b + 1] + ds, 0, 1 - 1e-12), temp,
+                                 min(max(top_p + dp, 1e-9), 1.0))
+                outs.add((int(n[0]), int(x[0])))
+    return outs, (int(base[0][0]), int(base[1][0]))
+
+
+def _verify_inputs(B, G, V, d_t, d_d, seed, o_std=4.0):
+    wl = WL.DecodeWorkload("t", B, G, V, d_d, d_t, o_std=o_std, seed=seed)
+    x = WL.make_decode_inputs(wl, device=DEV)
+    tl = x["o_target"].float() @ x["W_target"].float().T  # reference-side logits, not the HIP head
+    dl = x["o_draft"].float() @ x["W_draft"].float().T
+    tl = tl.reshape(B, G + 1, V).contiguous()
+    dl = dl.reshape(G, B, V).transpose(0, 1).contiguous()
+    return wl, x, dl, tl
+
+
+@pytest.mark.parametrize("B,G,V,temp,top_p", [(16, 4, 3000, 0.4, 0.9), (24, 6, 49152, 0.4, 0.9),
+                                               (10, 3, 1000, 1.0, 1.0), (8, 0, 5000, 0.4, 0.9),
+                                               (12, 5, 777, 0.8, 0.6)])
+def test_verify_parity(B, G, V, temp, top_p):
+    print(f"[decode] verify B={B} gamma={G} V={V} T={temp} p={top_p}", flush=True)
+    wl, x, dl, tl = _verify_inputs(B, G, V, 256, 128, seed=B * 31 + G)
+    dln, tln = _np(dl).astype(np.float64), _np(tl).astype(np.float64)
+    ua, us, ud = (_np(x["u_accept"]).astype(np.float64), _np(x["u_sample"]).astype(np.float64),
+                  _np(x["u_draft"]).astype(np.float64))
+    # drafted tokens: the oracle's draws from the draft distributions
+    drafts = np.zeros((B, G), dtype=np.int64)
+    for k in range(G):
+        drafts[:, k] = OD.sample(dln[:, k], ud[k], temp, top_p)
+    n_ref, x_ref = OD.verify(dln, tln, drafts, ua, us, temp, top_p)
+    n_gpu, x_gpu = D.spec_verify(dl if G > 0 else None, tl,
+                                 torch.tensor(drafts, dtype=torch.int32, device=DEV) if G > 0 else None,
+                                 x["u_accept"].contiguous() if G > 0 else None, x["u_sample"],
+                                 temperature=temp, top_p=top_p)
+    n_gpu, x_gpu = _np(n_gpu).astype(np.int64), _np(x_gpu).astype(np.int64)
+    miss = np.nonzero((n_gpu != n_ref) | (x_gpu != x_ref))[0]
+    for b in miss:
+        outs, base = _ambiguous_sequence(dln, tln, drafts, ua, us, temp, top_p, b)
+        assert (n_gpu[b], x_gpu[b]) in outs, (f"sequence {b}: GPU {(n_gpu[b], x_gpu[b])}, oracle "
+                                              f"{base}, under perturbation {sorted(outs)}")
+    assert len(miss) <= max(1, 0.05 * B), f"{len(miss)} ambiguous sequences"
+    if G > 0:
+        assert 0 < n_ref.sum() < B * G or B < 4  # the case exercises both outcomes
+
+
+def test_verify_greedy_matches_exactly():
+    B, G, V = 20, 5, 4000
+    wl, x, dl, tl = _verify_inputs(B, G, V, 256, 128, seed=77)
+    tln = _np(tl).astype(np.float64)
+    best = tln.argmax(axis=2)
+    drafts = best[:, :G].copy()
+    drafts[::3, 1] = (drafts[::3, 1] + 1) % V
+    drafts[1::4, 0] = (drafts[1::4, 0] + 2) % V
+    n_gpu, x_gpu = D.spec_verify(dl, tl, torch.tensor(drafts, dtype=torch.int32, device=DEV), None,
+                                 None, greedy=True)
+    n_ref, x_ref = OD.verify(_np(dl).astype(np.float64), tln, drafts, np.zeros((B, G)),
+                             np.zeros(B), 1.0, 1.0, greedy=True)
+    assert np.array_equal(_np(n_gpu), n_ref) and np.array_equal(_np(x_gpu), x_ref)
+
+
+def test_verify_rejection_draws_from_the_residual():
+    """With the draft certain of token 0 and the verifier uniform over 4 tokens,
+    token 0 is kept with probability 1/4 and the resampled tokens are 1, 2, 3
+    with equal frequency."""
+    N = 3000
+    dl = torch.full((N, 1, 4), -30.0, device=DEV)
+    dl[:, 0, 0] = 30.0
+    tl = torch.zeros(N, 2, 4, device=DEV)
+    drafts = torch.zeros(N, 1, dtype=torch.int32, device=DEV)
+    ua = ((torch.arange(N, device=DEV, dtype=torch.float32) * 0.618034) % 1.0)[:, None].contiguous()
+    us = (torch.arange(N, device=DEV, dtype=torch.float32) + 0.5) / N
+    n, x = D.spec_verify(dl, tl, drafts, ua, us, temperature=1.0, top_p=1.0)
+    n, x = _np(n), _np(x)
+    assert abs((n == 1).mean() - 0.25) < 0.01
+    rej = x[n == 0]
+    assert set(np.unique(rej)) <= {1, 2, 3}
+    freq = np.bincount(rej, minlength=4)[1:] / len(rej)
+    np.testing.assert_allclose(freq, 1 / 3, atol=0.02)
+
+
+def test_full_size_step():
+    """The 500M-draft / 3B-verifier step at batch 102 and the paper's vocabulary.
+    The head kernel is checked on sampled rows; sampling and verification are
+    then checked on reference logits (fp32 torch products, not the HIP head),
+    which both sides take as input."""
+    wl = WL.DECODE["spec_500m_3b"]
+    print(f"[decode] full-size step B={wl.batch} gamma={wl.gamma} V={wl.V}", flush=True)
+    x = WL.make_decode_inputs(wl, device=DEV)
+    B, G, V = wl.batch, wl.gamma, wl.V
+    tl = D.head_logits(x["o_target"], x["W_target"])
+    rows = np.random.default_rng(0).choice(B * (G + 1), 16, replace=False)
+    on = _np(x["o_target"][torch.from_numpy(rows).to(DEV)].float()).astype(np.float64)
+    Wn = _np(x["W_target"].float()).astype(np.float64)
+    ref = OD.head_logits(on, Wn)
+    got = _np(tl)[rows].astype(np.float64)
+    assert np.all(np.abs(got - ref) <= 1e-5 * (np.abs(on) @ np.abs(Wn).T) + 1e-6)
+    del tl
+    # reference logits for the sampling / verification parity
+    tlr = (x["o_target"].float() @ x["W_target"].float().T).reshape(B, G + 1, V).contiguous()
+    dlr = (x["o_draft"].float() @ x["W_draft"].float().T).reshape(G, B, V)
+    dln = _np(dlr.transpose(0, 1)).astype(np.float64)
+    tln = _np(tlr).astype(np.float64)
+    ud = _np(x["u_draft"]).astype(np.float64)
+    drafts = np.zeros((B, G), dtype=np.int64)
+    for k in range(G):
+        gpu_k = _np(D.sample(dlr[k].contiguous(), x["u_draft"][k].contiguous(),
+                             temperature=wl.temperature, top_p=wl.top_p)).astype(np.int64)
+        _check_samples(dln[:, k], ud[k], gpu_k, wl.temperature, wl.top_p)
+        drafts[:, k] = OD.sample(dln[:, k], ud[k], wl.temperature, wl.top_p)
+    ua, us = _np(x["u_accept"]).astype(np.float64), _np(x["u_sample"]).astype(np.float64)
+    n_gpu, x_gpu = D.spec_verify(dlr.transpose(0, 1).contiguous(), tlr,
+                                 torch.tensor(drafts, dtype=torch.int32, device=DEV),
+                                 x["u_accept"].contiguous(), x["u_sample"],
+                                 temperature=wl.temperature, top_p=wl.top_p)
+    n_ref, x_ref = OD.verify(dln, tln, drafts, ua, us, wl.temperature, wl.top_p)
+    n_gpu, x_gpu = _np(n_gpu), _np(x_gpu)
+    miss = np.nonzero((n_gpu != n_ref) | (x_gpu != x_ref))[0]
+    for b in miss:
+        outs, base = _ambiguous_sequence(dln, tln, drafts, ua, us, wl.temperature, wl.top_p, b)
+        assert (n_gpu[b], x_gpu[b]) in outs, (b, (n_gpu[b], x_gpu[b]), base)
+    assert len(miss) <= max(1, 0.05 * B)
+    print(f"[decode] mean accepted {n_ref.mean():.2f} of {G}", flush=True)
+
+
+def test_bitwise_deterministic():
+    g = torch.Generator(device=DEV).manual_seed(5)
+    logits = torch.randn(50, 49152, generator=g, device=DEV) * 2
+    u = torch.rand(50, generator=g, device=DEV)
+    a = D.sample(logits, u, temperature=0.4, top_p=0.9)
+    b = D.sample(logits, u, temperature=0.4, top_p=0.9)
+    assert torch.equal(a, b)
+
+
+def test_verify_empty_residual_draws_from_the_verifier():
+    dl = torch.tensor([[[0.0, 40.0, 0.0, 0.0]]], device=DEV)
+    tl = torch.tensor([[[0.0, 40.0, 0.0, 0.0], [0.0, 0.0, 0.0, 0.0]]], device=DEV)
+    n, x = D.spec_verify(dl, tl, torch.tensor([[3]], dtype=torch.int32, device=DEV),
+                         torch.tensor([[0.5]], device=DEV), torch.tensor([0.3], device=DEV),
+                         temperature=0.4, top_p=0.9)
+    assert _np(n).tolist() == [0] and _np(x).tolist() == [1]
+
+
+def test_verify_single_token_nuclei_accept_agreeing_drafts():
+    """Peaked rows whose scaled top logit is not exact in fp32 (37.3 / 0.4): every
+    weight recomputed from the logits must equal the one the distribution's
+    parameters were built from, so a draft equal to the verifier's only kept
+    token is always accepted."""
+    B, G, V = 4, 3, 3000
+    g = torch.Generator(device=DEV).manual_seed(3)
+    tl = torch.randn(B, G + 1, V, generator=g, device=DEV)
+    dl = torch.randn(B, G, V, generator=g, device=DEV)
+    top = torch.randint(0, V, (B, G + 1), generator=g, device=DEV)
+    tl.scatter_(2, top[:, :, None], 37.3)
+    dl.scatter_(2, top[:, :G, None], 37.3)
+    drafts = top[:, :G].to(torch.int32).contiguous()
+    ua = torch.full((B, G), 0.999, device=DEV)
+    us = torch.full((B,), 0.5, device=DEV)
+    n, x = D.spec_verify(dl, tl, drafts, ua, us, temperature=0.4, top_p=0.9)
+    assert _np(n).tolist() == [G] * B
+    assert _np(x).tolist() == _np(top[:, G]).tolist()
+    p = D.sample(tl[:, 0].contiguous(), us, temperature=0.4, top_p=0.9)
+    assert _np(p).tolist() == _np(top[:, 0]).tolist()

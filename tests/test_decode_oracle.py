@@ -229,3 +229,12 @@ def test_planted_mistake_is_caught(monkeypatch, name, filt, ver):
         except AssertionError:
             caught += 1
     assert caught > 0, f"mutant {name} passed every pin"
+
+
+def test_empty_residual_draws_from_the_verifier():
+    """Draft and verifier agree on a one-hot distribution and the drafted token
+    is impossible under both: it is rejected and the next token comes from p."""
+    dl = np.array([[[0.0, 40.0, 0.0, 0.0]]])
+    tl = np.array([[[0.0, 40.0, 0.0, 0.0], [0.0, 0.0, 0.0, 0.0]]])
+    n, x = OD.verify(dl, tl, np.array([[3]]), np.array([[0.5]]), np.array([0.3]), 0.4, 0.9)
+    assert n.tolist() == [0] and x.tolist() == [1]
