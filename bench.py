@@ -14,6 +14,12 @@ temperature 1 and top-1 agreement of every pair of sub-models).
 
 With --junction a step is the forward and backward of every inter-model junction
 (eq. (1)) of a suite (mls_junction_fwd + mls_junction_bwd per junction).
+
+With --decode a step is one speculative-decoding head step of a draft / verifier
+pair (section 3, "Speculative Decoding Throughput"): gamma draft steps (head logits
++ nucleus sampling for the batch), the verifier's head logits over the batch's
+gamma + 1 positions, and the verification (mls_head_logits, mls_sample,
+mls_spec_verify).
 """
 
 from __future__ import annotations
@@ -31,6 +37,8 @@ if ROOT not in sys.path:
 METRIC = "fused LM-head+CE+KL fwd+bwd tokens/s (M=3, V=50304); % of bf16 MFMA peak"
 METRIC_DIAG = "cross-model diagnostics (fused forward + pairwise KL/top-1 agreement) tokens/s"
 METRIC_JUNCTION = "inter-model junctions fwd+bwd tokens/s (every junction of the suite)"
+METRIC_DECODE = ("speculative head step rows/s (gamma draft steps x batch + verifier "
+                 "(gamma + 1) x batch rows)")
 PEAK_FLOPS = {"bf16": 2.5e15, "f32": 157.3e12}  # MI355X dense MFMA peaks
 HBM_PEAK = 8.0e12
 
@@ -81,6 +89,8 @@ def parse():
                     help="time the forward + pairwise diagnostics pass instead of fwd+bwd")
     ap.add_argument("--junction", action="store_true",
                     help="time the inter-model junctions (forward + backward) instead")
+    ap.add_argument("--decode", action="store_true",
+                    help="time the speculative-decoding head step instead")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB (a known-size "
                          "kernel to calibrate HBM byte counters)")
@@ -265,6 +275,172 @@ def main_junction(args):
     print(json.dumps(out), flush=True)
 
 
+def cpu_decode(wl, x, rows_req):
+    """Times the float64 oracle of the step (heads, draft draws, verification) on a
+    sample of sequences."""
+    import numpy as np
+    from oracle import decode as OD
+    B, G, V = wl.batch, wl.gamma, wl.V
+    Wt = x["W_target"].float().cpu().numpy()
+    Wd = x["W_draft"].float().cpu().numpy()
+    ot = x["o_target"].float().cpu().numpy().reshape(B, G + 1, -1)
+    od = x["o_draft"].float().cpu().numpy().reshape(G, B, -1)
+    ud = x["u_draft"].cpu().numpy()
+    ua = x["u_accept"].cpu().numpy()
+    us = x["u_sample"].cpu().numpy()
+
+    def run(n):
+        t0 = time.perf_counter()
+        dl = np.stack([OD.head_logits(od[k, :n], Wd) for k in range(G)], axis=1)  # [n, G, V]
+        drafts = np.stack([OD.sample(dl[:, k], ud[k, :n], wl.temperature, wl.top_p)
+                           for k in range(G)], axis=1)
+        tl = OD.head_logits(ot[:n].reshape(n * (G + 1), -1), Wt).reshape(n, G + 1, V)
+        OD.verify(dl, tl, drafts, ua[:n], us[:n], wl.temperature, wl.top_p)
+        return time.perf_counter() - t0
+
+    n = rows_req if rows_req > 0 else 2
+    while True:
+        dt = run(n)
+        log(f"oracle sample {n} sequences: {dt:.1f} s")
+        if rows_req > 0 or dt >= 10.0 or n >= B:
+            break
+        n = int(min(B, max(2 * n, n * 14.0 / max(dt, 1e-3))))
+    rows = n * G + n * (G + 1)
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()
+                       if p.get("user_api") == "blas"] or [os.cpu_count() or 1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    return {"value": rows / dt, "unit": "rows/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"float64 numpy oracle, the whole step for {n} of {B} sequences "
+                      f"({rows} rows); {dt:.1f} s"}
+
+
+def main_decode(args):
+    import torch
+    from paper_2608_09703_amd import binding as B
+    from paper_2608_09703_amd import workloads as WL
+
+    name = args.workload or "spec_500m_3b"
+    wl = WL.DECODE[name]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    Bt, G, V = wl.batch, wl.gamma, wl.V
+    log(f"decode workload {name}: batch={Bt} gamma={G} V={V} draft d={wl.d_draft} "
+        f"verifier d={wl.d_target} T={wl.temperature} top_p={wl.top_p}")
+    x = WL.make_decode_inputs(wl, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    sh = stream.cuda_stream
+    ldk = torch.empty(G, Bt, V, device=dev)         # draft logits, one slice per draft step
+    lt = torch.empty(Bt * (G + 1), V, device=dev)
+    tok = torch.empty(G, Bt, dtype=torch.int32, device=dev)
+    u_acc = x["u_accept"].t().contiguous()          # [gamma, batch], drafting order
+    n_acc = torch.empty(Bt, dtype=torch.int32, device=dev)
+    nxt = torch.empty(Bt, dtype=torch.int32, device=dev)
+    ws_b = B.spec_verify_workspace(Bt, G)
+    ws = torch.empty(ws_b, dtype=torch.uint8, device=dev)
+    samp = B.make_sampling(V, wl.temperature, wl.top_p)
+    od = x["o_draft"].reshape(G, Bt, -1)
+    cats = ["draft_head", "sample", "verify_head", "verify"]
+    ev = {c: [] for c in cats}
+
+    def mark(c, fn, timed):
+        if not timed:
+            fn()
+            return
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        fn()
+        b.record(stream)
+        ev[c].append((a, b))
+
+    def step(timed=False):
+        for k in range(G):
+            mark("draft_head", lambda: B.head_logits(Bt, V, wl.d_draft, B.MLS_BF16, od[k].data_ptr(),
+                                                     x["W_draft"].data_ptr(), ldk[k].data_ptr(), sh),
+                 timed)
+            mark("sample", lambda: B.sample(samp, Bt, ldk[k].data_ptr(), x["u_draft"][k].data_ptr(),
+                                            tok[k].data_ptr(), sh), timed)
+        mark("verify_head", lambda: B.head_logits(Bt * (G + 1), V, wl.d_target, B.MLS_BF16,
+                                                  x["o_target"].data_ptr(), x["W_target"].data_ptr(),
+                                                  lt.data_ptr(), sh), timed)
+        mark("verify", lambda: B.spec_verify(samp, Bt, G, ldk.data_ptr(), lt.data_ptr(),
+                                             tok.data_ptr(), u_acc.data_ptr(),
+                                             x["u_sample"].data_ptr(), n_acc.data_ptr(),
+                                             nxt.data_ptr(), ws.data_ptr(), ws_b, sh), timed)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(args.steps):
+        step(timed=True)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t0.elapsed_time(t1) / args.steps
+    per = {c: sum(a.elapsed_time(b) for a, b in ev[c]) / args.steps for c in cats}
+    rows = Bt * G + Bt * (G + 1)
+    log(f"{ms_step:.3f} ms/step, mean accepted {n_acc.float().mean().item():.2f} of {G}")
+    for c in cats:
+        log(f"  {c:12s} {per[c]:8.4f} ms/step")
+    # algorithmic work per step of each kernel category
+    dd, dt_ = wl.d_draft, wl.d_target
+    draft_bytes = G * (V * dd * 2 + Bt * dd * 2 + Bt * V * 4)
+    verify_flops = 2.0 * Bt * (G + 1) * V * dt_
+    verify_bytes = V * dt_ * 2 + Bt * (G + 1) * (dt_ * 2 + V * 4)
+    sample_bytes = G * (Bt * V * 4 + Bt * 8)
+    work = {
+        "draft_head": ("hbm", draft_bytes, HBM_PEAK, "GB/s", 1e9),
+        "verify_head": ("mfma", verify_flops, PEAK_FLOPS["bf16"], "TFLOP/s", 1e12)
+        if verify_flops / verify_bytes > PEAK_FLOPS["bf16"] / HBM_PEAK
+        else ("hbm", verify_bytes, HBM_PEAK, "GB/s", 1e9),
+        "sample": ("hbm", sample_bytes, HBM_PEAK, "GB/s", 1e9),
+    }
+    dom = max(work, key=lambda c: per[c])
+    bound, amount, peak, unit, scale = work[dom]
+    achieved = amount / (per[dom] / 1e3)
+    if args.copy_mib > 0:
+        src = torch.ones(args.copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_decode(wl, x, args.cpu_rows)
+    out = {
+        "metric": METRIC_DECODE,
+        "value": rows / (ms_step / 1e3),
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 heads and hidden states, fp32 logits and sampling",
+        "data": "synthetic (seeded nested draft/verifier heads and hidden states, input uniforms)",
+        "config": {"workload": name, "batch": Bt, "gamma": G, "V": V, "d_draft": dd,
+                   "d_verifier": dt_, "temperature": wl.temperature, "top_p": wl.top_p,
+                   "parallelism": "single GPU"},
+        "mean_accepted": n_acc.float().mean().item(),
+        "roofline": {"bound": bound, "kernel": dom, "achieved": achieved / scale,
+                     "peak": peak / scale, "unit": unit, "frac": achieved / peak,
+                     "traffic": profiled_traffic(name, {"draft_head": "head_logits",
+                                                        "verify_head": "head_logits"}.get(dom, dom),
+                                                 "decode")},
+        "ms_per_step_by_kernel": per,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -274,6 +450,8 @@ def main():
         sys.exit(2)
     if args.junction:
         return main_junction(args)
+    if args.decode:
+        return main_decode(args)
 
     import torch
     from paper_2608_09703_amd import binding as B

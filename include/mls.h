@@ -279,12 +279,13 @@ mls_status mls_spec_verify_workspace(int64_t batch, int64_t gamma, size_t* bytes
 
 /*
  * Speculative verification of `batch` sequences with `gamma` >= 0 drafted
- * tokens each (device arrays):
- *   draft_logits  [batch][gamma][V]      the draft's logits at each drafted position
- *   target_logits [batch][gamma + 1][V]  the verifier's logits at the same positions
- *                                        and the one after them
- *   draft_tokens  [batch][gamma] int32   the drafted tokens
- *   u_accept      [batch][gamma]         uniforms of the acceptance tests
+ * tokens each (device arrays). The draft's arrays are in drafting order, one
+ * [batch] slice per draft step, as a drafting loop produces them:
+ *   draft_logits  [gamma][batch][V]      the draft's logits at each drafted position
+ *   draft_tokens  [gamma][batch] int32   the drafted tokens
+ *   u_accept      [gamma][batch]         uniforms of the acceptance tests
+ *   target_logits [batch][gamma + 1][V]  the verifier's logits at the drafted positions
+ *                                        and the one after them (one pass per sequence)
  *   u_sample      [batch]                uniform of the final draw
  * Per sequence, drafted token x at position k is kept when
  * u_accept * q(x) < p(x) (q: the draft's sampling distribution, p: the

@@ -279,8 +279,9 @@ def spec_verify(draft_logits: Optional[torch.Tensor], target_logits: torch.Tenso
                 greedy: bool = False):
     """``(n_accepted [B], next_token [B])`` (int32) of speculative verification.
 
-    ``draft_logits [B, gamma, V]``, ``target_logits [B, gamma + 1, V]`` (fp32),
-    ``draft_tokens [B, gamma]`` (int32), ``u_accept [B, gamma]``, ``u_sample [B]``.
+    Draft-side arrays in drafting order: ``draft_logits [gamma, B, V]`` (fp32),
+    ``draft_tokens [gamma, B]`` (int32), ``u_accept [gamma, B]``; verifier side
+    ``target_logits [B, gamma + 1, V]`` (fp32) and ``u_sample [B]``.
     """
     Bt, G1, V = target_logits.shape
     G = G1 - 1
@@ -291,9 +292,11 @@ def spec_verify(draft_logits: Optional[torch.Tensor], target_logits: torch.Tenso
     if draft_tokens is not None and (draft_tokens.dtype != torch.int32 or
                                      not draft_tokens.is_contiguous()):
         raise ValueError("draft_tokens must be contiguous int32")
-    if G > 0 and (draft_logits is None or draft_logits.shape != (Bt, G, V) or
-                  draft_tokens is None or draft_tokens.shape != (Bt, G)):
-        raise ValueError("draft_logits [B, gamma, V] and draft_tokens [B, gamma] are required")
+    if G > 0 and (draft_logits is None or draft_logits.shape != (G, Bt, V) or
+                  draft_tokens is None or draft_tokens.shape != (G, Bt)):
+        raise ValueError("draft_logits [gamma, B, V] and draft_tokens [gamma, B] are required")
+    if G > 0 and not greedy and (u_accept is None or u_accept.shape != (G, Bt)):
+        raise ValueError("u_accept [gamma, B] is required")
     n_acc = torch.empty(Bt, dtype=torch.int32, device=dev)
     nxt = torch.empty(Bt, dtype=torch.int32, device=dev)
     ws_bytes = 0 if greedy else B.spec_verify_workspace(Bt, G)

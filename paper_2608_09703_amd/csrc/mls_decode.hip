@@ -120,7 +120,11 @@ __device__ __forceinline__ float weight_of(float scaled, float m) {
   return fast_exp2((scaled - m) * kLog2e);
 }
 
+constexpr int kMaxCand = 2048;  // nucleus candidates searched by one wave
+
 struct RowShared {
+  float cand[kMaxCand];       // compacted candidate weights (thread order)
+  int woff[kRowWaves];        // per-wave offsets of the compaction
   float red[kRowWaves];
   int ired[kRowWaves];
   float seg[kRowWaves * 64];  // per (slab, wave) partial sums for index-order scans
@@ -222,6 +226,7 @@ __device__ __forceinline__ int index_order_draw(Wt weight, float target, RowShar
   for (int i = 0; i < EPT; ++i) {
     const float s = wave_sum_f(weight(i));
     if (lane == 0) sh.seg[i * kRowWaves + wave] = s;
+    __builtin_amdgcn_sched_barrier(0);  // one reduction chain at a time
   }
   __syncthreads();
   // wave 0 scans the EPT * 16 segment sums in order (each lane owns a run of them)
@@ -329,15 +334,78 @@ __device__ __forceinline__ RowDist row_dist(const float* row, int V, float inv_t
   const float P = top_p * d.total;
   // largest bit pattern b with sum(e >= b) >= P; weights are in (0, 1]
   uint32_t lo = 0, hi = 0x3f800001u;  // sum(e >= 0) = total >= P; nothing is above 1
-  while (hi - lo > 1) {
-    const uint32_t mid = lo + (hi - lo) / 2;
-    float part = 0.f;
+  // Weights below c0 = (1 - top_p) total / V cannot decide the threshold: all V
+  // of them together hold at most (1 - top_p) of the mass, so sum(e >= c0) >= P
+  // and theta >= c0. The few weights at or above c0 are compacted into LDS and
+  // one wave bisects over them without block barriers.
+  const float c0 = (1.f - top_p) * d.total / (float)V;
+  const uint32_t b0 = __float_as_uint(c0);
+  int nc = 0;
+  float f0 = 0.f;
 #pragma unroll
-    for (int i = 0; i < EPT; ++i) part += __float_as_uint(e[i]) >= mid ? e[i] : 0.f;
-    if (block_sum(part, sh) >= P)
-      lo = mid;
-    else
-      hi = mid;
+  for (int i = 0; i < EPT; ++i) {
+    const bool c = __float_as_uint(e[i]) >= b0 && e[i] > 0.f;
+    nc += c ? 1 : 0;
+    f0 += c ? e[i] : 0.f;
+  }
+  // exclusive prefix of the candidate counts in thread order
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  int incl = nc;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int up = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += up;
+  }
+  if (lane == 63) sh.woff[wave] = incl;
+  const float F0 = block_sum(f0, sh);  // (also orders the woff writes before the reads)
+  int base = 0, n_cand = 0;
+#pragma unroll
+  for (int w = 0; w < kRowWaves; ++w) {
+    base += w < wave ? sh.woff[w] : 0;
+    n_cand += sh.woff[w];
+  }
+  if (F0 >= P && b0 > 0 && n_cand <= kMaxCand) {
+    int pos = base + incl - nc;
+#pragma unroll
+    for (int i = 0; i < EPT; ++i)
+      if (__float_as_uint(e[i]) >= b0 && e[i] > 0.f) sh.cand[pos++] = e[i];
+    __syncthreads();
+    if (wave == 0) {
+      constexpr int PER = kMaxCand / 64;
+      float cv[PER];
+#pragma unroll
+      for (int q = 0; q < PER; ++q) {
+        const int k = q * 64 + lane;
+        cv[q] = k < n_cand ? sh.cand[k] : 0.f;
+      }
+      uint32_t wlo = b0, whi = hi;  // sum(e >= b0) = F0 >= P
+      while (whi - wlo > 1) {
+        const uint32_t mid = wlo + (whi - wlo) / 2;
+        float part = 0.f;
+#pragma unroll
+        for (int q = 0; q < PER; ++q) part += __float_as_uint(cv[q]) >= mid ? cv[q] : 0.f;
+        if (wave_sum_f(part) >= P)
+          wlo = mid;
+        else
+          whi = mid;
+      }
+      if (lane == 0) sh.ibcast[2] = (int)wlo;
+    }
+    __syncthreads();
+    lo = (uint32_t)sh.ibcast[2];
+    __syncthreads();
+  } else {
+    while (hi - lo > 1) {
+      const uint32_t mid = lo + (hi - lo) / 2;
+      float part = 0.f;
+#pragma unroll
+      for (int i = 0; i < EPT; ++i) part += __float_as_uint(e[i]) >= mid ? e[i] : 0.f;
+      if (block_sum(part, sh) >= P)
+        lo = mid;
+      else
+        hi = mid;
+    }
   }
   d.theta = __uint_as_float(lo);
   float above = 0.f;
@@ -503,7 +571,7 @@ __global__ __launch_bounds__(kRowThreads) void verify_kernel(VerifyArgs a) {
   int k = 0;
   int next = 0;
   for (; k < G; ++k) {
-    const int x = a.draft_tokens[b * G + k];
+    const int x = a.draft_tokens[(int64_t)k * a.batch + b];
     const float* trow = a.target_logits + (b * (G + 1) + k) * a.V;
     if (a.greedy) {
       const int best = row_argmax<EPT>(trow, V, sh);
@@ -513,13 +581,13 @@ __global__ __launch_bounds__(kRowThreads) void verify_kernel(VerifyArgs a) {
       }
       continue;
     }
-    const float* drow = a.draft_logits + (b * G + k) * a.V;
-    const RowDist dq = a.params[b * G + k];
+    const float* drow = a.draft_logits + ((int64_t)k * a.batch + b) * a.V;
+    const RowDist dq = a.params[(int64_t)k * a.batch + b];
     const RowDist dp = a.params[a.batch * G + b * (G + 1) + k];
     const bool in = x >= 0 && x < V;
     const float qx = in ? prob_at(drow, x, it, dq) : 0.f;
     const float px = in ? prob_at(trow, x, it, dp) : 0.f;
-    if (a.u_accept[b * G + k] * qx < px) continue;
+    if (a.u_accept[(int64_t)k * a.batch + b] * qx < px) continue;
     // rejected: draw from max(0, p - q)
     auto res = [&](int i) {
       const int v = threadIdx.x + kRowThreads * i;

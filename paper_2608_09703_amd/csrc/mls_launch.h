@@ -213,17 +213,17 @@ struct RowParamArgs {
   RowDist* params;        // [rows0 + rows1]
 };
 struct VerifyArgs {
-  const RowDist* params;  // draft rows [batch][gamma], then verifier rows [batch][gamma + 1]
+  const RowDist* params;  // draft rows [gamma][batch], then verifier rows [batch][gamma + 1]
   int64_t batch;
   int64_t V;
   int32_t gamma;
   int32_t greedy;
   float inv_temp;
   float top_p;
-  const float* draft_logits;   // [batch][gamma][V]
+  const float* draft_logits;   // [gamma][batch][V] (one row per draft step and sequence)
   const float* target_logits;  // [batch][gamma + 1][V]
-  const int32_t* draft_tokens; // [batch][gamma]
-  const float* u_accept;       // [batch][gamma]
+  const int32_t* draft_tokens; // [gamma][batch]
+  const float* u_accept;       // [gamma][batch]
   const float* u_sample;       // [batch]
   int32_t* n_accepted;         // [batch]
   int32_t* next_token;         // [batch]

@@ -179,10 +179,13 @@ class DecodeWorkload:
     sequences, draft length gamma, nucleus 0.9 at temperature 0.4).
 
     The draft's head and hidden states are the leading ``d_draft`` columns of
-    the verifier's (nested sub-models share their leading parameters), so the
-    two distributions are related as a draft and its verifier are. Hidden states
-    are N(0, o_std^2), heads N(0, w_std^2); with these values the temperature-0.4
-    distributions are peaked (nuclei of a few to a few hundred tokens).
+    the verifier's (nested sub-models share their leading parameters). The
+    verifier's hidden states are N(0, o_std^2) on those columns and
+    N(0, (tail_scale * o_std)^2) on the rest, and the draft's are the verifier's
+    leading columns plus N(0, (draft_noise * o_std)^2): the draft then agrees
+    with its verifier about as a distilled draft does (per-token acceptance
+    around 0.7 at temperature 0.4, nuclei of tens of tokens). Heads are
+    N(0, w_std^2).
     """
 
     name: str
@@ -193,7 +196,9 @@ class DecodeWorkload:
     d_target: int
     temperature: float = 0.4
     top_p: float = 0.9
-    o_std: float = 4.0
+    o_std: float = 3.0
+    tail_scale: float = 0.15
+    draft_noise: float = 0.05
     w_std: float = 0.02
     seed: int = 0
 
@@ -212,15 +217,16 @@ def make_decode_inputs(wl: DecodeWorkload, device="cpu", seed: Optional[int] = N
     step-major), uniforms of the draft draws [gamma, batch], of the acceptance
     tests [batch, gamma] and of the final draws [batch]. The draft's hidden
     state at (step k, sequence b) is the leading d_draft columns of the
-    verifier's at the same position plus N(0, (o_std / 2)^2) noise.
+    verifier's at the same position plus the noise.
     """
     g = torch.Generator(device=device)
     g.manual_seed(wl.seed if seed is None else seed)
     B, G = wl.batch, wl.gamma
     Wt = (torch.randn(wl.V, wl.d_target, generator=g, device=device) * wl.w_std).to(torch.bfloat16)
-    ot = (torch.randn(B * (G + 1), wl.d_target, generator=g, device=device) * wl.o_std).to(
-        torch.bfloat16)
-    noise = torch.randn(G * B, wl.d_draft, generator=g, device=device) * (wl.o_std / 2)
+    ot = torch.randn(B * (G + 1), wl.d_target, generator=g, device=device) * wl.o_std
+    ot[:, wl.d_draft:] *= wl.tail_scale
+    ot = ot.to(torch.bfloat16)
+    noise = torch.randn(G * B, wl.d_draft, generator=g, device=device) * (wl.o_std * wl.draft_noise)
     pos = (torch.arange(B, device=device)[None, :] * (G + 1) + torch.arange(G, device=device)[:, None])
     od = (ot[pos.reshape(-1), :wl.d_draft].float() + noise).to(torch.bfloat16)
     u_draft = torch.rand(G, B, generator=g, device=device)

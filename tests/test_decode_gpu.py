@@ -161,8 +161,8 @@ def _ambiguous_sequence(dl, tl, drafts, ua, us, temp, top_p, b):
     return outs, (int(base[0][0]), int(base[1][0]))
 
 
-def _verify_inputs(B, G, V, d_t, d_d, seed, o_std=4.0):
-    wl = WL.DecodeWorkload("t", B, G, V, d_d, d_t, o_std=o_std, seed=seed)
+def _verify_inputs(B, G, V, d_t, d_d, seed):
+    wl = WL.DecodeWorkload("t", B, G, V, d_d, d_t, seed=seed)
     x = WL.make_decode_inputs(wl, device=DEV)
     tl = x["o_target"].float() @ x["W_target"].float().T  # reference-side logits, not the HIP head
     dl = x["o_draft"].float() @ x["W_draft"].float().T
@@ -185,9 +185,10 @@ def test_verify_parity(B, G, V, temp, top_p):
     for k in range(G):
         drafts[:, k] = OD.sample(dln[:, k], ud[k], temp, top_p)
     n_ref, x_ref = OD.verify(dln, tln, drafts, ua, us, temp, top_p)
-    n_gpu, x_gpu = D.spec_verify(dl if G > 0 else None, tl,
-                                 torch.tensor(drafts, dtype=torch.int32, device=DEV) if G > 0 else None,
-                                 x["u_accept"].contiguous() if G > 0 else None, x["u_sample"],
+    n_gpu, x_gpu = D.spec_verify(dl.transpose(0, 1).contiguous() if G > 0 else None, tl,
+                                 torch.tensor(drafts.T.copy(), dtype=torch.int32, device=DEV)
+                                 if G > 0 else None,
+                                 x["u_accept"].t().contiguous() if G > 0 else None, x["u_sample"],
                                  temperature=temp, top_p=top_p)
     n_gpu, x_gpu = _np(n_gpu).astype(np.int64), _np(x_gpu).astype(np.int64)
     miss = np.nonzero((n_gpu != n_ref) | (x_gpu != x_ref))[0]
@@ -208,7 +209,8 @@ def test_verify_greedy_matches_exactly():
     drafts = best[:, :G].copy()
     drafts[::3, 1] = (drafts[::3, 1] + 1) % V
     drafts[1::4, 0] = (drafts[1::4, 0] + 2) % V
-    n_gpu, x_gpu = D.spec_verify(dl, tl, torch.tensor(drafts, dtype=torch.int32, device=DEV), None,
+    n_gpu, x_gpu = D.spec_verify(dl.transpose(0, 1).contiguous(), tl,
+                                 torch.tensor(drafts.T.copy(), dtype=torch.int32, device=DEV), None,
                                  None, greedy=True)
     n_ref, x_ref = OD.verify(_np(dl).astype(np.float64), tln, drafts, np.zeros((B, G)),
                              np.zeros(B), 1.0, 1.0, greedy=True)
@@ -220,11 +222,11 @@ def test_verify_rejection_draws_from_the_residual():
     token 0 is kept with probability 1/4 and the resampled tokens are 1, 2, 3
     with equal frequency."""
     N = 3000
-    dl = torch.full((N, 1, 4), -30.0, device=DEV)
-    dl[:, 0, 0] = 30.0
+    dl = torch.full((1, N, 4), -30.0, device=DEV)
+    dl[0, :, 0] = 30.0
     tl = torch.zeros(N, 2, 4, device=DEV)
-    drafts = torch.zeros(N, 1, dtype=torch.int32, device=DEV)
-    ua = ((torch.arange(N, device=DEV, dtype=torch.float32) * 0.618034) % 1.0)[:, None].contiguous()
+    drafts = torch.zeros(1, N, dtype=torch.int32, device=DEV)
+    ua = ((torch.arange(N, device=DEV, dtype=torch.float32) * 0.618034) % 1.0)[None, :].contiguous()
     us = (torch.arange(N, device=DEV, dtype=torch.float32) + 0.5) / N
     n, x = D.spec_verify(dl, tl, drafts, ua, us, temperature=1.0, top_p=1.0)
     n, x = _np(n), _np(x)
@@ -265,9 +267,9 @@ def test_full_size_step():
         _check_samples(dln[:, k], ud[k], gpu_k, wl.temperature, wl.top_p)
         drafts[:, k] = OD.sample(dln[:, k], ud[k], wl.temperature, wl.top_p)
     ua, us = _np(x["u_accept"]).astype(np.float64), _np(x["u_sample"]).astype(np.float64)
-    n_gpu, x_gpu = D.spec_verify(dlr.transpose(0, 1).contiguous(), tlr,
-                                 torch.tensor(drafts, dtype=torch.int32, device=DEV),
-                                 x["u_accept"].contiguous(), x["u_sample"],
+    n_gpu, x_gpu = D.spec_verify(dlr.contiguous(), tlr,
+                                 torch.tensor(drafts.T.copy(), dtype=torch.int32, device=DEV),
+                                 x["u_accept"].t().contiguous(), x["u_sample"],
                                  temperature=wl.temperature, top_p=wl.top_p)
     n_ref, x_ref = OD.verify(dln, tln, drafts, ua, us, wl.temperature, wl.top_p)
     n_gpu, x_gpu = _np(n_gpu), _np(x_gpu)
@@ -312,7 +314,8 @@ def test_verify_single_token_nuclei_accept_agreeing_drafts():
     drafts = top[:, :G].to(torch.int32).contiguous()
     ua = torch.full((B, G), 0.999, device=DEV)
     us = torch.full((B,), 0.5, device=DEV)
-    n, x = D.spec_verify(dl, tl, drafts, ua, us, temperature=0.4, top_p=0.9)
+    n, x = D.spec_verify(dl.transpose(0, 1).contiguous(), tl, drafts.t().contiguous(),
+                         ua.t().contiguous(), us, temperature=0.4, top_p=0.9)
     assert _np(n).tolist() == [G] * B
     assert _np(x).tolist() == _np(top[:, G]).tolist()
     p = D.sample(tl[:, 0].contiguous(), us, temperature=0.4, top_p=0.9)
