@@ -432,9 +432,7 @@ def main_decode(args):
         "mean_accepted": n_acc.float().mean().item(),
         "roofline": {"bound": bound, "kernel": dom, "achieved": achieved / scale,
                      "peak": peak / scale, "unit": unit, "frac": achieved / peak,
-                     "traffic": profiled_traffic(name, {"draft_head": "head_logits",
-                                                        "verify_head": "head_logits"}.get(dom, dom),
-                                                 "decode")},
+                     "traffic": profiled_traffic(name, dom, "decode")},
         "ms_per_step_by_kernel": per,
         "cpu_baseline": cpu,
     }
