@@ -82,7 +82,7 @@ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-constexpr int64_t kSlabTargetBytes = 512ll << 20;  // logit-gradient slab(s) per chunk
+constexpr int64_t kSlabTargetBytes = 4ll << 30;  // logit-gradient slab(s) per chunk
 
 struct Plan {
   int M = 0;

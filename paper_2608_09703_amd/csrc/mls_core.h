@@ -33,6 +33,15 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 __device__ __forceinline__ void block_barrier() { __builtin_amdgcn_s_barrier(); }
 
+// Barrier after which other waves may overwrite LDS this wave has read: the
+// wave's own LDS reads are drained first (s_barrier itself waits for nothing,
+// and direct-to-LDS loads issued by other waves after the barrier reach LDS
+// through the vector memory path, unordered with respect to reads still queued).
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+}
+
 // Blocks are dispatched round-robin over the 8 XCDs of the chip; this gives
 // each XCD a contiguous range of logical tile indices (a bijection on
 // [0, nb)), so tiles that share operand panels share one L2.
@@ -336,7 +345,9 @@ struct WideMma {
       } else {
         wait_vmcnt<0>();
       }
-      block_barrier();
+      // stage (kt - 1) % STAGES is refilled below: every wave's reads of it must
+      // have completed
+      stage_barrier();
       const int nt = kt + STAGES - 1;
       if (nt < nk) {
         char* st = smem + (nt % STAGES) * kStageBytes;
@@ -349,7 +360,7 @@ struct WideMma {
       const char* stage = smem + (kt % STAGES) * kStageBytes;
       compute_stage(stage, stage + BM * RB, lane, wm, wn);
     }
-    block_barrier();
+    stage_barrier();
   }
 
   __device__ __forceinline__ static int row_of(int wm, int fm, int r, int lane) {

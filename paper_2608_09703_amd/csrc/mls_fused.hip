@@ -399,7 +399,7 @@ __global__ __launch_bounds__(Mma::NT, MINB) void fused_bwd_wide_kernel(FusedArgs
           __builtin_amdgcn_sched_barrier(0);  // bound live ranges: one 4-row group at a time
         }
     }
-    block_barrier();
+    stage_barrier();  // the staged tile is complete before any wave copies it out
 
     // 2. token-major slab: BN rows x kChunks chunks of 16 bytes
     uint16_t* slab = static_cast<uint16_t*>(a.slab) + (int64_t)i * a.T_pad * a.Vc;
@@ -411,7 +411,7 @@ __global__ __launch_bounds__(Mma::NT, MINB) void fused_bwd_wide_kernel(FusedArgs
       const uint4 v = *reinterpret_cast<const uint4*>(smem + t * kGRow + ((c ^ (t & kCMask)) << 4));
       *reinterpret_cast<uint4*>(slab + (tbase + t) * a.Vc + vloc + c * 8) = v;
     }
-    block_barrier();  // the stage memory is reused by the next tile product
+    stage_barrier();  // the stage memory is refilled by the next tile product
   }
 }
 

@@ -61,15 +61,33 @@ struct RowState {
   float xr[kMaxModels];
 };
 
+// arr[s] for a runtime s, with compile-time indices (keeps arr in registers)
+template <typename X>
+__device__ __forceinline__ X pick(const X* arr, int s) {
+  X r = arr[0];
+#pragma unroll
+  for (int i = 1; i < kMaxModels; ++i)
+    if (i == s) r = arr[i];
+  return r;
+}
+
 __device__ __forceinline__ void absorb(RowState& st, int M, int s, float ct, const float4* rec) {
-  // rec[i] = partial of sub-model i (same vocabulary range for all i)
-  const float ms_old = st.m[s];
-  const float ms_new = fmaxf(ms_old, rec[s].x);
+  // rec[i] = partial of sub-model i (same vocabulary range for all i). The
+  // teacher's entries are picked with compile-time indices so that rec and st
+  // stay in registers.
+  float ms_old = 0.f, rs_x = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxModels; ++i)
+    if (i == s) {
+      ms_old = st.m[i];
+      rs_x = rec[i].x;
+    }
+  const float ms_new = fmaxf(ms_old, rs_x);
   const float wa = fast_exp2((ms_old - ms_new) * ct);
-  const float wb = fast_exp2((rec[s].x - ms_new) * ct);
+  const float wb = fast_exp2((rs_x - ms_new) * ct);
 #pragma unroll
   for (int i = 0; i < kMaxModels; ++i) {
-    if (i >= M) break;
+    if (i >= M) continue;  // (not break: keeps the loop fully unrolled)
     const float mo = st.m[i];
     const float mn = fmaxf(mo, rec[i].x);
     st.s1[i] = st.s1[i] * fast_exp2((mo - mn) * kLog2e) + rec[i].y * fast_exp2((rec[i].x - mn) * kLog2e);
@@ -79,8 +97,8 @@ __device__ __forceinline__ void absorb(RowState& st, int M, int s, float ct, con
   }
 }
 
-constexpr int kRowTok = 64;   // tokens per block
-constexpr int kRowGrp = 4;    // partial groups per token
+constexpr int kRowTok = 16;   // tokens per block
+constexpr int kRowGrp = 16;   // partial groups per token (merged in a fixed order)
 
 __global__ __launch_bounds__(kThreads) void finalize_rows_kernel(RowArgs a) {
   __shared__ float4 sh[kRowGrp - 1][kRowTok][kMaxModels];
@@ -101,6 +119,7 @@ __global__ __launch_bounds__(kThreads) void finalize_rows_kernel(RowArgs a) {
     st.xr[i] = 0.f;
   }
   if (t < a.T) {
+#pragma unroll 4
     for (int j = grp; j < a.n_vt; j += kRowGrp) {
       float4 rec[kMaxModels];
 #pragma unroll
@@ -121,7 +140,7 @@ __global__ __launch_bounds__(kThreads) void finalize_rows_kernel(RowArgs a) {
 #pragma unroll
     for (int i = 0; i < kMaxModels; ++i)
       if (i < M) rec[i] = sh[g2][tl][i];
-    if (rec[s].x == -INFINITY) continue;  // group saw no tile
+    if (pick(rec, s).x == -INFINITY) continue;  // group saw no tile
     absorb(st, M, s, ct, rec);
   }
 
@@ -133,19 +152,20 @@ __global__ __launch_bounds__(kThreads) void finalize_rows_kernel(RowArgs a) {
   float* ce_row = a.stats + 2 * (int64_t)M * T;
   float* kl_row = a.stats + 3 * (int64_t)M * T;
   float* h_row = a.stats + 4 * (int64_t)M * T;
-  const float lset_s = st.m[s] * inv_tau + logf(st.st[s]);
-  const float den = a.tau * st.st[s];
+  const float m_s = pick(st.m, s), st_s = pick(st.st, s), xr_s = pick(st.xr, s);
+  const float lset_s = m_s * inv_tau + logf(st_s);
+  const float den = a.tau * st_s;
 #pragma unroll
   for (int i = 0; i < kMaxModels; ++i) {
-    if (i >= M) break;
+    if (i >= M) continue;
     const float l1 = st.m[i] + logf(st.s1[i]);
     const float lt = st.m[i] * inv_tau + logf(st.st[i]);
     lse1[i * T + t] = l1;
     lset[i * T + t] = lt;
     ce_row[i * T + t] = valid ? l1 - a.lab[i * T + t] : 0.f;
-    kl_row[i * T + t] = (valid && i != s) ? (st.xr[s] - st.xr[i]) / den - lset_s + lt : 0.f;
+    kl_row[i * T + t] = (valid && i != s) ? (xr_s - st.xr[i]) / den - lset_s + lt : 0.f;
   }
-  h_row[t] = valid ? lset_s - st.xr[s] / den : 0.f;
+  h_row[t] = valid ? lset_s - xr_s / den : 0.f;
 }
 
 __device__ __forceinline__ double wave_sum(double v) {
@@ -175,7 +195,7 @@ __global__ __launch_bounds__(kRedThreads) void reduce_losses_kernel(RowArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < kMaxModels; ++i) {
-      if (i >= M) break;
+      if (i >= M) continue;
       acc[i] += ce_row[i * T + t];
       acc[kMaxModels + i] += kl_row[i * T + t];
     }

@@ -220,3 +220,27 @@ def test_reduced_T_full_head_gradient(name):
         tail = (wl.V // 256) * 256
         if tail < wl.V:
             assert_grad(gpu["grad_W"][i][tail:], gW[i][tail:], f"{name} grad_W[{i}] tail")
+
+
+@pytest.mark.parametrize("name", ["c3_m3_v128k_tau2"])
+def test_full_size_backward_is_bitwise_repeatable(name):
+    """Three backward passes at full size (two vocabulary chunks of up to 87k rows)
+    give bitwise identical gradients, and every row of the logit gradient sums to
+    zero in each (grad_W column sums vanish)."""
+    wl = WL.WORKLOADS[name]
+    print(f"[repeat] {name}", flush=True)
+    h, W, y = WL.make_inputs(wl, device=DEV)
+    g_ce, g_kl = _coeffs(wl.M, -1, wl.alpha, wl.tau)
+    first = None
+    for rep in range(3):
+        gpu = run_gpu(h, W, y, tau=wl.tau, g_ce=g_ce, g_kl=g_kl)
+        for i in range(wl.M):
+            colsum = gpu["grad_W"][i].astype(np.float64).sum(axis=0)
+            scale = np.abs(gpu["grad_W"][i]).astype(np.float64).sum(axis=0).max()
+            assert np.abs(colsum).max() <= 1e-3 * scale, (rep, i)
+        if first is None:
+            first = gpu
+            continue
+        for i in range(wl.M):
+            assert np.array_equal(gpu["grad_W"][i], first["grad_W"][i]), (rep, i)
+            assert np.array_equal(gpu["grad_h"][i], first["grad_h"][i]), (rep, i)
