@@ -46,6 +46,8 @@ SMALL = [
     ("c1_small_f32", WL.WORKLOADS["c1_small_f32"], -1, 1.0, "paper", 0),
     ("f32_ragged", WL.custom(3, 150, (32, 36, 100), 555, dtype="f32", tau=1.5, w_std=0.1,
                              ignore_frac=0.1, seed=8), -1, 0.4, "paper", 256),
+    ("m8_max_models", WL.custom(8, 200, (64, 64, 128, 128, 192, 256, 256, 320), 700, tau=1.5,
+                                w_std=0.05, ignore_frac=0.1, seed=9), 5, 0.6, "paper", 256),
 ]
 
 
