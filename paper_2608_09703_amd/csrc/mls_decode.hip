@@ -29,6 +29,7 @@
 #include "mls_core.h"
 #include "mls_device.h"
 #include "mls_launch.h"
+#include "mls_wave.h"
 
 namespace mls {
 
@@ -103,9 +104,55 @@ __global__ __launch_bounds__(Mma::NT, 2) void head_logits_kernel(HeadArgs a) {
 // ---------------------------------------------------------------------------
 // 2./3. per-row sampling distribution
 // ---------------------------------------------------------------------------
+//
+// One 1024-thread block per row. Element i of a thread sits at vocabulary
+// index v = 64 EPT wave + 64 i + lane: each wave owns a contiguous range of
+// 64 EPT tokens, a slab i of it is one coalesced 256-byte load, and index
+// order is (wave, slab, lane).
+//
+// Nucleus threshold. With `total` the sum of the row's exp weights and
+// P = top_p * total, theta is the largest weight value whose mass
+// S(theta) = sum(weight >= theta) still reaches P. Two facts bound it:
+// * S(c) >= P implies theta >= c (theta is the largest such value);
+// * for c' > c, S(c') >= S(c) - n(c) c', where n(c) counts the weights at or
+//   above c; so S(c) >= P also gives theta >= (S(c) - P) / n(c).
+// The search starts at c0 = (1 - top_p) total / V (the weights below c0 hold
+// less than (1 - top_p) of the mass, so S(c0) >= P) and raises the bound with
+// the second fact while the candidate set {weight >= c} is large. The
+// candidates are then compacted into LDS in index order, and one wave bisects
+// the fp32 bit pattern over them (positive floats order like their bits),
+// resolves ties and draws: every kept token is a candidate. Rows whose
+// candidate set stays large (flat distributions) take a block-wide search
+// over the whole row.
 
 constexpr int kRowThreads = 1024;
 constexpr int kRowWaves = kRowThreads / 64;
+constexpr int kMaxEPT = 64;
+constexpr int kRunMax = 16;              // candidate entries per lane of the list wave
+constexpr int kMaxCand = 64 * kRunMax;   // candidates one wave holds
+constexpr int kSmallCand = 4 * 64;       // lists searched with 4 entries per lane
+constexpr int kBigCand = 4 * kRowThreads;  // first list: 4 entries per thread
+constexpr int kRegion = kBigCand / kRowWaves;  // first-list entries per wave
+constexpr int kBoundRounds = 3;          // raises of the lower bound
+
+// LDS slot of list entry j: one gap after every 16 entries, so that the lanes
+// of the list wave, each reading a run of consecutive entries, hit different
+// banks.
+__device__ __forceinline__ int cand_slot(int j) { return j + (j >> 4); }
+constexpr int kCandSlots = kMaxCand + kMaxCand / 16;
+
+struct RowShared {
+  float bw[kBigCand];             // first list (weights >= c0), index order
+  int bi[kBigCand];
+  float cw[kCandSlots];           // final list, index order
+  int ci[kCandSlots];             // their vocabulary indices
+  float seg[kMaxEPT * kRowWaves]; // per (slab, wave) sums for whole-row index-order scans
+  float red[kRowWaves];
+  int ired[kRowWaves];
+  int wcnt[kRowWaves];            // per-wave list counts
+  float bcast[4];
+  int ibcast[4];
+};
 
 // A row's exp weights are formed in several places (the distribution's
 // parameters, then draws and probabilities recomputed from the logits); they
@@ -120,37 +167,9 @@ __device__ __forceinline__ float weight_of(float scaled, float m) {
   return fast_exp2((scaled - m) * kLog2e);
 }
 
-constexpr int kMaxCand = 2048;  // nucleus candidates searched by one wave
-
-struct RowShared {
-  float cand[kMaxCand];       // compacted candidate weights (thread order)
-  int woff[kRowWaves];        // per-wave offsets of the compaction
-  float red[kRowWaves];
-  int ired[kRowWaves];
-  float seg[kRowWaves * 64];  // per (slab, wave) partial sums for index-order scans
-  float bcast[4];
-  int ibcast[4];
-};
-
-__device__ __forceinline__ float wave_sum_f(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-__device__ __forceinline__ int wave_sum_i(int v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-__device__ __forceinline__ float wave_max_f(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
-}
-
 // Block-wide reductions in a fixed order (every thread gets the result).
 __device__ __forceinline__ float block_sum(float v, RowShared& sh) {
-  v = wave_sum_f(v);
+  v = wave_sum(v);
   const int w = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) sh.red[w] = v;
   __syncthreads();
@@ -161,7 +180,7 @@ __device__ __forceinline__ float block_sum(float v, RowShared& sh) {
   return s;
 }
 __device__ __forceinline__ int block_count(int v, RowShared& sh) {
-  v = wave_sum_i(v);
+  v = wave_sum(v);
   const int w = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) sh.ired[w] = v;
   __syncthreads();
@@ -171,8 +190,48 @@ __device__ __forceinline__ int block_count(int v, RowShared& sh) {
   __syncthreads();
   return s;
 }
+__device__ __forceinline__ void block_sum2(float& f, int& n, RowShared& sh) {
+  f = wave_sum(f);
+  n = wave_sum(n);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    sh.red[w] = f;
+    sh.ired[w] = n;
+  }
+  __syncthreads();
+  float s = 0.f;
+  int c = 0;
+#pragma unroll
+  for (int i = 0; i < kRowWaves; ++i) {
+    s += sh.red[i];
+    c += sh.ired[i];
+  }
+  __syncthreads();
+  f = s;
+  n = c;
+}
+// As block_sum2, with n already the wave's total in every lane.
+__device__ __forceinline__ void block_sum2w(float& f, int& n, RowShared& sh) {
+  f = wave_sum(f);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    sh.red[w] = f;
+    sh.ired[w] = n;
+  }
+  __syncthreads();
+  float s = 0.f;
+  int c = 0;
+#pragma unroll
+  for (int i = 0; i < kRowWaves; ++i) {
+    s += sh.red[i];
+    c += sh.ired[i];
+  }
+  __syncthreads();
+  f = s;
+  n = c;
+}
 __device__ __forceinline__ float block_max(float v, RowShared& sh) {
-  v = wave_max_f(v);
+  v = wave_max(v);
   const int w = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) sh.red[w] = v;
   __syncthreads();
@@ -185,15 +244,7 @@ __device__ __forceinline__ float block_max(float v, RowShared& sh) {
 
 // Argmax with the lowest index on ties.
 __device__ __forceinline__ void block_argmax(float& val, int& idx, RowShared& sh) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const float ov = __shfl_xor(val, o, 64);
-    const int oi = __shfl_xor(idx, o, 64);
-    if (ov > val || (ov == val && oi < idx)) {
-      val = ov;
-      idx = oi;
-    }
-  }
+  wave_argmax(val, idx);
   const int w = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) {
     sh.red[w] = val;
@@ -204,19 +255,51 @@ __device__ __forceinline__ void block_argmax(float& val, int& idx, RowShared& sh
   idx = sh.ired[0];
 #pragma unroll
   for (int i = 1; i < kRowWaves; ++i)
-    if (sh.red[i] > val || (sh.red[i] == val && sh.ired[i] < idx)) {
+    if (argmax_better(sh.red[i], sh.ired[i], val, idx)) {
       val = sh.red[i];
       idx = sh.ired[i];
     }
   __syncthreads();
 }
 
-// The thread's element i sits at vocabulary index v = threadIdx.x + kRowThreads * i
-// (slab i), so index order is (slab, wave, lane).
+// Vocabulary index of the thread's element i.
+template <int EPT>
+__device__ __forceinline__ int elem_v(int i) {
+  return (int)(threadIdx.x >> 6) * (64 * EPT) + 64 * i + (int)(threadIdx.x & 63);
+}
 
-// Smallest index whose cumulative weight in index order exceeds `target`;
-// weight(i) gives the thread's i-th weight. Returns -1 if the total does not
-// exceed it.
+// Number of the thread's elements inside the row: element i exists iff
+// i < elems_in_row (a compare with a constant, so no per-element index needs
+// to stay live).
+template <int EPT>
+__device__ __forceinline__ int elems_in_row(int V) {
+  const int v0 = elem_v<EPT>(0);
+  return V > v0 ? (V - v0 + 63) >> 6 : 0;
+}
+
+// The thread's EPT logits of a row, x[i] = row[elem_v(i)], as buffer loads
+// over the row's V * 4 bytes: one per-lane offset, the slab as a scalar
+// offset, and indices past the row read 0 from the hardware range check, so
+// every load is unconditional and all of them are in flight together.
+// Callers mask v >= V themselves.
+template <int EPT>
+__device__ __forceinline__ void load_row(const float* row, int V, float* x) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)row, (short)0, V * 4, 0x00020000);
+  const int base = elem_v<EPT>(0) * 4;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i)
+    x[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, base, 256 * i, 0));
+}
+
+__device__ __forceinline__ int lanes_below(unsigned long long m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32),
+                                        __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+}
+
+// Smallest index whose cumulative weight in index order exceeds `target`,
+// over the whole row; weight(i) gives the thread's i-th weight. Returns -1 if
+// the total does not exceed it.
 template <int EPT, class Wt>
 __device__ __forceinline__ int index_order_draw(Wt weight, float target, RowShared& sh) {
   const int wave = threadIdx.x >> 6;
@@ -224,33 +307,25 @@ __device__ __forceinline__ int index_order_draw(Wt weight, float target, RowShar
   // per (slab, wave) sums
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
-    const float s = wave_sum_f(weight(i));
-    if (lane == 0) sh.seg[i * kRowWaves + wave] = s;
-    __builtin_amdgcn_sched_barrier(0);  // one reduction chain at a time
+    const float s = wave_sum(weight(i));
+    if (lane == 0) sh.seg[wave * EPT + i] = s;
   }
   __syncthreads();
-  // wave 0 scans the EPT * 16 segment sums in order (each lane owns a run of them)
+  // wave 0 scans the 16 EPT segment sums in index order (each lane owns a run of them)
   if (wave == 0) {
     constexpr int NSEG = EPT * kRowWaves;
-    constexpr int PER = (NSEG + 63) / 64;
+    constexpr int PER = NSEG / 64;
     float run = 0.f;
-    for (int q = 0; q < PER; ++q) {
-      const int sidx = lane * PER + q;
-      run += sidx < NSEG ? sh.seg[sidx] : 0.f;
-    }
-    // exclusive prefix of the lanes' runs
-    float incl = run;
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const float up = __shfl_up(incl, o, 64);
-      if (lane >= o) incl += up;
-    }
+    for (int q = 0; q < PER; ++q) run += sh.seg[lane * PER + q];
+    const float incl = wave_incl_scan(run);
     float before = incl - run;
     int found = -1;
     float found_before = 0.f;
+#pragma unroll
     for (int q = 0; q < PER; ++q) {
       const int sidx = lane * PER + q;
-      const float s = sidx < NSEG ? sh.seg[sidx] : 0.f;
+      const float s = sh.seg[sidx];
       if (found < 0 && s > 0.f && before + s > target) {
         found = sidx;
         found_before = before;
@@ -259,11 +334,8 @@ __device__ __forceinline__ int index_order_draw(Wt weight, float target, RowShar
     }
     // the first lane (in index order) that found its segment wins
     const unsigned long long m = __ballot(found >= 0);
-    const int first = m ? __ffsll((long long)m) - 1 : -1;
-    if (lane == 0) {
-      sh.ibcast[0] = -1;
-    }
-    if (first >= 0 && lane == first) {
+    if (lane == 0) sh.ibcast[0] = -1;
+    if (m && lane == __builtin_ctzll(m)) {
       sh.ibcast[0] = found;
       sh.bcast[0] = found_before;
     }
@@ -273,27 +345,24 @@ __device__ __forceinline__ int index_order_draw(Wt weight, float target, RowShar
   const float base = sh.bcast[0];
   __syncthreads();
   if (sidx < 0) return -1;
-  const int slab = sidx / kRowWaves;
-  const int swave = sidx % kRowWaves;
+  const int swave = sidx / EPT;
+  const int slab = sidx % EPT;
   // inside the segment: the owning wave scans its 64 lanes
   if (wave == swave) {
     float x = 0.f;
 #pragma unroll
     for (int i = 0; i < EPT; ++i)
       if (i == slab) x = weight(i);
-    float incl = x;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const float up = __shfl_up(incl, o, 64);
-      if (lane >= o) incl += up;
-    }
+    const float incl = wave_incl_scan(x);
     const unsigned long long m = __ballot(x > 0.f && base + incl > target);
-    int pick = m ? __ffsll((long long)m) - 1 : -1;
-    if (pick < 0) {  // rounding: take the last positive weight of the segment
+    int pick;
+    if (m) {
+      pick = __builtin_ctzll(m);
+    } else {  // rounding: take the last positive weight of the segment
       const unsigned long long pos = __ballot(x > 0.f);
-      pick = pos ? 63 - __clzll((long long)pos) : 0;
+      pick = pos ? 63 - __builtin_clzll(pos) : 0;
     }
-    if (lane == 0) sh.ibcast[1] = slab * kRowThreads + swave * 64 + pick;
+    if (lane == 0) sh.ibcast[1] = swave * (64 * EPT) + slab * 64 + pick;
   }
   __syncthreads();
   const int v = sh.ibcast[1];
@@ -301,22 +370,287 @@ __device__ __forceinline__ int index_order_draw(Wt weight, float target, RowShar
   return v;
 }
 
-
 __device__ __forceinline__ bool kept_w(float e, int v, const RowDist& d) {
   return e > d.theta || (e == d.theta && e > 0.f && v <= d.tie_cut);
 }
 
-// Loads a row and computes its sampling distribution; `e` receives the exp
-// weights exp(l / T - max) of the thread's elements (0 beyond V).
+// Writes the row elements with flag(i) set to an LDS list in index order
+// (weight val(i) to dw, vocabulary index to di; at cand_slot(position) when
+// PAD) and returns how many there are; entries beyond CAP are not written.
+// Index order is (wave, slab, lane): a first pass counts each wave's
+// elements, then every wave writes from the sum of the counts before it.
+template <int EPT, int CAP, bool PAD, class Flag, class Val>
+__device__ __forceinline__ int compact_row(Flag flag, Val val, float* dw, int* di,
+                                           RowShared& sh) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  int cnt = 0;  // wave-uniform
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) cnt += __builtin_popcountll(__ballot(flag(i)));
+  if (lane == 0) sh.wcnt[wave] = cnt;
+  __syncthreads();
+  int pos0 = 0, total = 0;
+#pragma unroll
+  for (int k = 0; k < kRowWaves; ++k) {
+    pos0 += k < wave ? sh.wcnt[k] : 0;
+    total += sh.wcnt[k];
+  }
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    const bool f = flag(i);
+    const unsigned long long b = __ballot(f);
+    if (f) {
+      const int pos = pos0 + lanes_below(b);
+      if (pos < CAP) {
+        const int sl = PAD ? cand_slot(pos) : pos;
+        dw[sl] = val(i);
+        di[sl] = elem_v<EPT>(i);
+      }
+    }
+    pos0 += __builtin_popcountll(b);
+  }
+  __syncthreads();
+  return total;
+}
+
+// One pass: each wave writes its flagged elements, in index order, to its own
+// region of kRegion entries of the first list (bw, bi); the counts go to
+// sh.wcnt. Returns the total; `fits` tells whether every wave's elements fit
+// its region.
+template <int EPT, class Flag, class Val>
+__device__ __forceinline__ int compact_regions(Flag flag, Val val, RowShared& sh, bool& fits) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  int pos0 = 0;  // wave-uniform
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    const bool f = flag(i);
+    const unsigned long long b = __ballot(f);
+    if (f) {
+      const int pos = pos0 + lanes_below(b);
+      if (pos < kRegion) {
+        sh.bw[wave * kRegion + pos] = val(i);
+        sh.bi[wave * kRegion + pos] = elem_v<EPT>(i);
+      }
+    }
+    pos0 += __builtin_popcountll(b);
+  }
+  if (lane == 0) sh.wcnt[wave] = pos0;
+  __syncthreads();
+  int total = 0;
+  fits = true;
+#pragma unroll
+  for (int k = 0; k < kRowWaves; ++k) {
+    total += sh.wcnt[k];
+    fits = fits && sh.wcnt[k] <= kRegion;
+  }
+  return total;
+}
+
+// ---- list wave (wave 0, all lanes active): lane l holds entries [l RUN, (l + 1) RUN)
+
+template <int RUN>
+__device__ __forceinline__ void load_run(const RowShared& sh, int n, float (&w)[RUN]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int q = 0; q < RUN; ++q) {
+    const int j = lane * RUN + q;
+    w[q] = j < n ? sh.cw[cand_slot(j)] : 0.f;
+  }
+}
+
+template <int RUN>
+__device__ __forceinline__ int run_index(const RowShared& sh, int q) {
+  return sh.ci[cand_slot((int)(threadIdx.x & 63) * RUN + q)];
+}
+
+// Position in the list of the first entry (index order) whose cumulative
+// weight exceeds `target`; the last positive entry when rounding leaves the
+// target at or above the sum; 0 when every weight is 0 (a kept set never is
+// empty: the largest weight is 1 and theta <= 1).
+template <int RUN>
+__device__ __forceinline__ int run_draw(const float (&kw)[RUN], float target) {
+  const int lane = threadIdx.x & 63;
+  float run = 0.f;
+#pragma unroll
+  for (int q = 0; q < RUN; ++q) run += kw[q];
+  const float incl = wave_incl_scan(run);
+  const unsigned long long hit = __ballot(run > 0.f && incl > target);
+  const unsigned long long pos = __ballot(run > 0.f);
+  if (!pos) return 0;
+  const int L = hit ? __builtin_ctzll(hit) : 63 - __builtin_clzll(pos);
+  int j = 0;
+  if (lane == L) {
+    float acc = incl - run;
+    int first = -1, last = 0;
+#pragma unroll
+    for (int q = 0; q < RUN; ++q) {
+      if (kw[q] > 0.f) {
+        acc += kw[q];
+        last = q;
+        if (first < 0 && acc > target) first = q;
+      }
+    }
+    j = lane * RUN + (first >= 0 ? first : last);
+  }
+  return __builtin_amdgcn_readlane(j, L);
+}
+
+// Theta from the final list (list wave; n entries, weights >= c with
+// S(c) >= P): the largest bit pattern whose mass reaches P. Four-way steps:
+// three probes, three independent reductions. The probed sets are nested and
+// summed in the same order, so the computed masses are ordered like the exact
+// ones and the decisions are consistent. Theta is a list value: once a single
+// entry remains in [lo, hi), it is theta.
+template <int RUN>
+__device__ __forceinline__ float list_theta(const float (&w)[RUN], float c, float P) {
+  const int lane = threadIdx.x & 63;
+  // invariant: S(lo) >= P > S(hi); lo, hi and the decisions are wave-uniform
+  uint32_t lo = __float_as_uint(c), hi = 0x3f800001u;  // nothing is above 1
+  while (hi - lo > 1) {
+    int inside = 0;
+    float last = 0.f;
+#pragma unroll
+    for (int q = 0; q < RUN; ++q) {
+      const uint32_t b = __float_as_uint(w[q]);
+      const bool in = b >= lo && b < hi;
+      inside += in ? 1 : 0;
+      last = in ? w[q] : last;
+    }
+    const unsigned long long any = __ballot(inside > 0);
+    if (__builtin_popcountll(any) == 1 && __ballot(inside > 1) == 0) {
+      const float v = __builtin_bit_cast(
+          float, __builtin_amdgcn_readlane(__float_as_int(last), __builtin_ctzll(any)));
+      return v;
+    }
+    if (hi - lo > 3) {
+      const uint32_t st = (hi - lo) >> 2;
+      const uint32_t m1 = lo + st, m2 = m1 + st, m3 = m2 + st;
+      float p1 = 0.f, p2 = 0.f, p3 = 0.f;
+#pragma unroll
+      for (int q = 0; q < RUN; ++q) {
+        const uint32_t b = __float_as_uint(w[q]);
+        p1 += b >= m1 ? w[q] : 0.f;
+        p2 += b >= m2 ? w[q] : 0.f;
+        p3 += b >= m3 ? w[q] : 0.f;
+      }
+      const int g1 = __builtin_amdgcn_readfirstlane(wave_sum(p1) >= P ? 1 : 0);
+      const int g2 = __builtin_amdgcn_readfirstlane(wave_sum(p2) >= P ? 1 : 0);
+      const int g3 = __builtin_amdgcn_readfirstlane(wave_sum(p3) >= P ? 1 : 0);
+      if (g3) {
+        lo = m3;
+      } else if (g2) {
+        lo = m2;
+        hi = m3;
+      } else if (g1) {
+        lo = m1;
+        hi = m2;
+      } else {
+        hi = m1;
+      }
+    } else {
+      const uint32_t mid = lo + (hi - lo) / 2;
+      float part = 0.f;
+#pragma unroll
+      for (int q = 0; q < RUN; ++q) part += __float_as_uint(w[q]) >= mid ? w[q] : 0.f;
+      if (__builtin_amdgcn_readfirstlane(wave_sum(part) >= P ? 1 : 0))
+        lo = mid;
+      else
+        hi = mid;
+    }
+  }
+  (void)lane;
+  return __uint_as_float(lo);
+}
+
+// Completes a row's distribution from its final list (list wave): theta, the
+// tie cut and the kept mass. `kw` receives the kept weights of the lane's run.
+template <int RUN>
+__device__ __forceinline__ void run_dist(const RowShared& sh, int n, float c, float P, int V,
+                                         RowDist& d, float (&kw)[RUN]) {
+  const int lane = threadIdx.x & 63;
+  float w[RUN];
+  load_run<RUN>(sh, n, w);
+  const float th = list_theta<RUN>(w, c, P);
+  d.theta = th;
+  float above = 0.f;
+  int ties = 0;
+#pragma unroll
+  for (int q = 0; q < RUN; ++q) {
+    above += w[q] > th ? w[q] : 0.f;
+    ties += w[q] == th ? 1 : 0;  // th > 0, so padding zeros never tie
+  }
+  const float mass_above = wave_sum(above);
+  const int n_tie = wave_sum(ties);
+  int k = n_tie;
+  if (n_tie > 1) {
+    k = (int)ceilf((P - mass_above) / th);
+    k = k < 1 ? 1 : (k > n_tie ? n_tie : k);
+  }
+  d.tie_cut = V;
+  if (k < n_tie) {  // vocabulary index of the k-th tied entry (the list is in index order)
+    const int incl = wave_incl_scan(ties);
+    const int L = __builtin_ctzll(__ballot(incl >= k));
+    int cut = 0;
+    if (lane == L) {
+      int seen = incl - ties;
+#pragma unroll
+      for (int q = 0; q < RUN; ++q)
+        if (w[q] == th && ++seen == k) cut = run_index<RUN>(sh, q);
+    }
+    d.tie_cut = __builtin_amdgcn_readlane(cut, L);
+  }
+  float kp = 0.f;
+#pragma unroll
+  for (int q = 0; q < RUN; ++q) {
+    kw[q] = w[q] > th || (w[q] == th && run_index<RUN>(sh, q) <= d.tie_cut) ? w[q] : 0.f;
+    kp += kw[q];
+  }
+  d.kept = wave_sum(kp);
+}
+
+// Mass and count of the weights at or above t (block-wide).
 template <int EPT>
-__device__ __forceinline__ RowDist row_dist(const float* row, int V, float inv_temp, float top_p, float* e,
-                            RowShared& sh) {
-  RowDist d;
+__device__ __forceinline__ void mass_at(const float* e, float t, float& F, int& n, RowShared& sh) {
+  F = 0.f;
+  n = 0;  // per wave: the same in every lane
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    const bool in = e[i] >= t;
+    F += in ? e[i] : 0.f;
+    n += __builtin_popcountll(__ballot(in));
+  }
+  block_sum2w(F, n, sh);
+}
+
+// Mass and count of the list entries w[] >= t held by the threads (block-wide).
+__device__ __forceinline__ void list_mass(const float (&w)[4], float t, float& F, int& n,
+                                          RowShared& sh) {
+  F = 0.f;
+  n = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    F += w[q] >= t ? w[q] : 0.f;
+    n += w[q] >= t ? 1 : 0;
+  }
+  block_sum2(F, n, sh);
+}
+
+// Loads a row and computes its sampling distribution. `e` receives the
+// thread's exp weights exp(l / T - max) (0 beyond V). With a nucleus and a
+// small candidate set the candidates (weights >= `c`) are left in the LDS
+// list and their number is returned: then only m and total are set in d, and
+// the list wave completes it (run_dist). Otherwise the whole distribution is
+// in d for every thread and -1 is returned.
+template <int EPT>
+__device__ __forceinline__ int row_dist(const float* row, int V, float inv_temp, float top_p,
+                                        float* e, RowShared& sh, RowDist& d, float& c, float& P) {
+  load_row<EPT>(row, V, e);
+  const int nv = elems_in_row<EPT>(V);
   float mx = -INFINITY;
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
-    const int v = threadIdx.x + kRowThreads * i;
-    e[i] = v < V ? scaled_logit(row[v], inv_temp) : -INFINITY;
+    e[i] = i < nv ? scaled_logit(e[i], inv_temp) : -INFINITY;
     mx = fmaxf(mx, e[i]);
   }
   d.m = block_max(mx, sh);
@@ -330,82 +664,100 @@ __device__ __forceinline__ RowDist row_dist(const float* row, int V, float inv_t
   d.theta = 0.f;
   d.tie_cut = V;
   d.kept = d.total;
-  if (!(top_p < 1.f)) return d;
-  const float P = top_p * d.total;
-  // largest bit pattern b with sum(e >= b) >= P; weights are in (0, 1]
+  if (!(top_p < 1.f)) return -1;
+  P = top_p * d.total;
+  c = (1.f - top_p) * d.total / (float)V;
+  bool ok = c > 0.f;
+  if (ok) {
+    const float c0 = c;
+    bool fits;
+    compact_regions<EPT>([&](int i) { return e[i] >= c0; }, [&](int i) { return e[i]; }, sh,
+                         fits);
+    if (fits) {
+      // the bound rounds run on the first list: the thread holds entries 4 lane
+      // .. 4 lane + 3 of its wave's region, so thread order is index order
+      const int lane = threadIdx.x & 63;
+      const int wave = threadIdx.x >> 6;
+      const int nw = sh.wcnt[wave];
+      float w[4];
+      int ix[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int j = 4 * lane + q;
+        w[q] = j < nw ? sh.bw[wave * kRegion + j] : 0.f;
+        ix[q] = sh.bi[wave * kRegion + j];
+      }
+      float F;
+      int n;
+      list_mass(w, c, F, n, sh);
+      ok = F >= P;
+      for (int r = 0; ok && r < kBoundRounds && n > kSmallCand; ++r) {
+        const float t = (F - P) / (float)n;
+        if (!(t > c)) break;
+        float F2;
+        int n2;
+        list_mass(w, t, F2, n2, sh);
+        if (!(F2 >= P)) break;
+        c = t;
+        F = F2;
+        n = n2;
+      }
+      if (ok && n <= kMaxCand) {  // stable compaction of the weights >= c into the final list
+        int cnt = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) cnt += w[q] >= c ? 1 : 0;
+        const int incl = wave_incl_scan(cnt);
+        if (lane == 63) sh.ired[wave] = incl;
+        __syncthreads();
+        int pos = incl - cnt;
+#pragma unroll
+        for (int k = 0; k < kRowWaves; ++k) pos += k < wave ? sh.ired[k] : 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (w[q] >= c) {
+            sh.cw[cand_slot(pos)] = w[q];
+            sh.ci[cand_slot(pos)] = ix[q];
+            ++pos;
+          }
+        __syncthreads();
+        return n;
+      }
+    } else {
+      // a large first list: the rounds run over the thread's row elements
+      float F;
+      int n;
+      mass_at<EPT>(e, c, F, n, sh);
+      ok = F >= P;
+      for (int r = 0; ok && r < kBoundRounds && n > kSmallCand; ++r) {
+        const float t = (F - P) / (float)n;
+        if (!(t > c)) break;
+        float F2;
+        int n2;
+        mass_at<EPT>(e, t, F2, n2, sh);
+        if (!(F2 >= P)) break;
+        c = t;
+        F = F2;
+        n = n2;
+      }
+      if (ok && n <= kMaxCand) {
+        const float cc = c;
+        return compact_row<EPT, kMaxCand, true>([&](int i) { return e[i] >= cc; },
+                                                [&](int i) { return e[i]; }, sh.cw, sh.ci, sh);
+      }
+    }
+  }
+  // whole-row search: largest bit pattern b with sum(e >= b) >= P
   uint32_t lo = 0, hi = 0x3f800001u;  // sum(e >= 0) = total >= P; nothing is above 1
-  // Weights below c0 = (1 - top_p) total / V cannot decide the threshold: all V
-  // of them together hold at most (1 - top_p) of the mass, so sum(e >= c0) >= P
-  // and theta >= c0. The few weights at or above c0 are compacted into LDS and
-  // one wave bisects over them without block barriers.
-  const float c0 = (1.f - top_p) * d.total / (float)V;
-  const uint32_t b0 = __float_as_uint(c0);
-  int nc = 0;
-  float f0 = 0.f;
+  if (ok) lo = __float_as_uint(c);  // S(c) >= P was checked
+  while (hi - lo > 1) {
+    const uint32_t mid = lo + (hi - lo) / 2;
+    float part = 0.f;
 #pragma unroll
-  for (int i = 0; i < EPT; ++i) {
-    const bool c = __float_as_uint(e[i]) >= b0 && e[i] > 0.f;
-    nc += c ? 1 : 0;
-    f0 += c ? e[i] : 0.f;
-  }
-  // exclusive prefix of the candidate counts in thread order
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  int incl = nc;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int up = __shfl_up(incl, o, 64);
-    if (lane >= o) incl += up;
-  }
-  if (lane == 63) sh.woff[wave] = incl;
-  const float F0 = block_sum(f0, sh);  // (also orders the woff writes before the reads)
-  int base = 0, n_cand = 0;
-#pragma unroll
-  for (int w = 0; w < kRowWaves; ++w) {
-    base += w < wave ? sh.woff[w] : 0;
-    n_cand += sh.woff[w];
-  }
-  if (F0 >= P && b0 > 0 && n_cand <= kMaxCand) {
-    int pos = base + incl - nc;
-#pragma unroll
-    for (int i = 0; i < EPT; ++i)
-      if (__float_as_uint(e[i]) >= b0 && e[i] > 0.f) sh.cand[pos++] = e[i];
-    __syncthreads();
-    if (wave == 0) {
-      constexpr int PER = kMaxCand / 64;
-      float cv[PER];
-#pragma unroll
-      for (int q = 0; q < PER; ++q) {
-        const int k = q * 64 + lane;
-        cv[q] = k < n_cand ? sh.cand[k] : 0.f;
-      }
-      uint32_t wlo = b0, whi = hi;  // sum(e >= b0) = F0 >= P
-      while (whi - wlo > 1) {
-        const uint32_t mid = wlo + (whi - wlo) / 2;
-        float part = 0.f;
-#pragma unroll
-        for (int q = 0; q < PER; ++q) part += __float_as_uint(cv[q]) >= mid ? cv[q] : 0.f;
-        if (wave_sum_f(part) >= P)
-          wlo = mid;
-        else
-          whi = mid;
-      }
-      if (lane == 0) sh.ibcast[2] = (int)wlo;
-    }
-    __syncthreads();
-    lo = (uint32_t)sh.ibcast[2];
-    __syncthreads();
-  } else {
-    while (hi - lo > 1) {
-      const uint32_t mid = lo + (hi - lo) / 2;
-      float part = 0.f;
-#pragma unroll
-      for (int i = 0; i < EPT; ++i) part += __float_as_uint(e[i]) >= mid ? e[i] : 0.f;
-      if (block_sum(part, sh) >= P)
-        lo = mid;
-      else
-        hi = mid;
-    }
+    for (int i = 0; i < EPT; ++i) part += __float_as_uint(e[i]) >= mid ? e[i] : 0.f;
+    if (block_sum(part, sh) >= P)
+      lo = mid;
+    else
+      hi = mid;
   }
   d.theta = __uint_as_float(lo);
   float above = 0.f;
@@ -419,8 +771,7 @@ __device__ __forceinline__ RowDist row_dist(const float* row, int V, float inv_t
   const int n_tie = block_count(ties, sh);
   int k = n_tie;
   if (n_tie > 1 && d.theta > 0.f) {
-    const float need = P - mass_above;
-    k = (int)ceilf(need / d.theta);
+    k = (int)ceilf((P - mass_above) / d.theta);
     k = k < 1 ? 1 : (k > n_tie ? n_tie : k);
   }
   // index of the k-th tied token (counts are exact in fp32 up to 2^24)
@@ -432,21 +783,21 @@ __device__ __forceinline__ RowDist row_dist(const float* row, int V, float inv_t
   float kp = 0.f;
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
-    const int v = threadIdx.x + kRowThreads * i;
+    const int v = elem_v<EPT>(i);
     kp += kept_w(e[i], v, d) ? e[i] : 0.f;
   }
   d.kept = block_sum(kp, sh);
-  return d;
+  return -1;
 }
 
-// Draw from a row's distribution with uniform u (weights in `e`, parameters in
-// d); `e` is overwritten with the kept weights.
+// Whole-row draw from a row's distribution with uniform u (weights in `e`,
+// parameters in d); `e` is overwritten with the kept weights.
 template <int EPT>
 __device__ __forceinline__ int row_draw(float* e, const RowDist& d, float u, RowShared& sh) {
   int last = -1;
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
-    const int v = threadIdx.x + kRowThreads * i;
+    const int v = elem_v<EPT>(i);
     e[i] = kept_w(e[i], v, d) ? e[i] : 0.f;
     if (e[i] > 0.f) last = v;
   }
@@ -462,38 +813,35 @@ __device__ __forceinline__ int row_draw(float* e, const RowDist& d, float u, Row
 
 template <int EPT>
 __device__ __forceinline__ int row_argmax(const float* row, int V, RowShared& sh) {
+  float x[EPT];
+  load_row<EPT>(row, V, x);
+  const int nv = elems_in_row<EPT>(V);
   float best = -INFINITY;
   int bi = 0x7fffffff;
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
-    const int v = threadIdx.x + kRowThreads * i;
-    if (v < V) {
-      const float x = row[v];
-      if (x > best) {  // v increases with i: strict > keeps the lowest index
-        best = x;
-        bi = v;
-      }
+    if (i < nv && x[i] > best) {  // the index increases with i: strict > keeps the lowest
+      best = x[i];
+      bi = i;
     }
   }
+  bi = bi == 0x7fffffff ? bi : elem_v<EPT>(0) + 64 * bi;
   block_argmax(best, bi, sh);
   return bi;
 }
 
-// Normalised probability of token x under a row's distribution (0 outside [0, V)).
-template <int EPT>
-__device__ __forceinline__ float weight_at(const float* e, const RowDist& d, int x, int V, RowShared& sh) {
-  if (x >= 0 && x < V && (x % kRowThreads) == (int)threadIdx.x) {
-    const int i = x / kRowThreads;
-    float w = 0.f;
-#pragma unroll
-    for (int j = 0; j < EPT; ++j)
-      if (j == i) w = kept_w(e[j], x, d) ? e[j] : 0.f;
-    sh.bcast[2] = w / d.kept;
-  }
-  __syncthreads();
-  const float r = (x >= 0 && x < V) ? sh.bcast[2] : 0.f;
-  __syncthreads();
-  return r;
+// The distribution from the final list (every thread calls it; only wave 0
+// works, the other waves return -2 at once), then (with u >= 0) a draw;
+// returns the drawn token (or -1 without a draw).
+template <int RUN>
+__device__ __forceinline__ int list_finish(RowShared& sh, int n, float c, float P, int V,
+                                           float u, RowDist& d) {
+  if (threadIdx.x >= 64) return -2;
+  float kw[RUN];
+  run_dist<RUN>(sh, n, c, P, V, d, kw);
+  if (u < 0.f) return -1;
+  const int j = run_draw<RUN>(kw, u * d.kept);
+  return sh.ci[cand_slot(j)];
 }
 
 template <int EPT>
@@ -506,8 +854,16 @@ __global__ __launch_bounds__(kRowThreads) void sample_kernel(SampleArgs a) {
     tok = row_argmax<EPT>(row, (int)a.V, sh);
   } else {
     float e[EPT];
-    const RowDist d = row_dist<EPT>(row, (int)a.V, a.inv_temp, a.top_p, e, sh);
-    tok = row_draw<EPT>(e, d, a.u[r], sh);
+    RowDist d;
+    float c = 0.f, P = 0.f;
+    const int n = row_dist<EPT>(row, (int)a.V, a.inv_temp, a.top_p, e, sh, d, c, P);
+    if (n >= 0) {
+      tok = n <= kSmallCand ? list_finish<4>(sh, n, c, P, (int)a.V, a.u[r], d)
+                            : list_finish<kRunMax>(sh, n, c, P, (int)a.V, a.u[r], d);
+      if (threadIdx.x >= 64) return;
+    } else {
+      tok = row_draw<EPT>(e, d, a.u[r], sh);
+    }
   }
   if (threadIdx.x == 0) a.tokens[r] = tok;
 }
@@ -520,7 +876,16 @@ __global__ __launch_bounds__(kRowThreads) void row_params_kernel(RowParamArgs a)
   const int64_t r = blockIdx.x;
   const float* row = r < a.rows0 ? a.logits0 + r * a.V : a.logits1 + (r - a.rows0) * a.V;
   float e[EPT];
-  const RowDist d = row_dist<EPT>(row, (int)a.V, a.inv_temp, a.top_p, e, sh);
+  RowDist d;
+  float c = 0.f, P = 0.f;
+  const int n = row_dist<EPT>(row, (int)a.V, a.inv_temp, a.top_p, e, sh, d, c, P);
+  if (n >= 0) {
+    if (n <= kSmallCand)
+      list_finish<4>(sh, n, c, P, (int)a.V, -1.f, d);
+    else
+      list_finish<kRunMax>(sh, n, c, P, (int)a.V, -1.f, d);
+    if (threadIdx.x >= 64) return;
+  }
   if (threadIdx.x == 0) a.params[r] = d;
 }
 
@@ -536,12 +901,13 @@ __device__ __forceinline__ float prob_at(const float* row, int v, float inv_temp
   return kept_w(e, v, d) ? e / d.kept : 0.f;
 }
 
-// Draw with uniform u from a row's distribution, weights recomputed from the logits.
+// Whole-row draw with uniform u from a row's distribution, weights recomputed
+// from the logits.
 template <int EPT>
 __device__ __forceinline__ int draw_kept(const float* row, int V, float it, const RowDist& d,
                                          float u, RowShared& sh) {
   auto w = [&](int i) {
-    const int v = threadIdx.x + kRowThreads * i;
+    const int v = elem_v<EPT>(i);
     if (v >= V) return 0.f;
     const float e = exp_weight(row[v], it, d);
     return kept_w(e, v, d) ? e : 0.f;
@@ -550,7 +916,7 @@ __device__ __forceinline__ int draw_kept(const float* row, int V, float it, cons
   if (v < 0) {
     int last = -1;
     for (int i = 0; i < EPT; ++i)
-      if (w(i) > 0.f) last = threadIdx.x + kRowThreads * i;
+      if (w(i) > 0.f) last = elem_v<EPT>(i);
     float lv = (float)last;
     block_argmax(lv, last, sh);
     v = last;
@@ -558,10 +924,54 @@ __device__ __forceinline__ int draw_kept(const float* row, int V, float it, cons
   return v;
 }
 
+// Compacts the kept tokens of row p (weights recomputed from the logits) into
+// the LDS list; returns their number.
+template <int EPT>
+__device__ __forceinline__ int compact_kept(const float* prow, int V, float it, const RowDist& dp,
+                                            RowShared& sh) {
+  float w[EPT];
+  load_row<EPT>(prow, V, w);
+  const int nv = elems_in_row<EPT>(V);
+  const int v0 = elem_v<EPT>(0);
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    const float e = exp_weight(w[i], it, dp);
+    w[i] = i < nv && kept_w(e, v0 + 64 * i, dp) ? e : 0.f;
+  }
+  return compact_row<EPT, kMaxCand, true>([&](int i) { return w[i] > 0.f; },
+                                          [&](int i) { return w[i]; }, sh.cw, sh.ci, sh);
+}
+
+// List wave: a draw from p's kept list (n entries) with uniform u; with a
+// draft row qrow (parameters dq), from max(0, p - q), or p itself if that has
+// no mass.
+template <int RUN>
+__device__ __forceinline__ int list_residual_draw(const RowShared& sh, int n, const RowDist& dp,
+                                                  const float* qrow, const RowDist& dq, float it,
+                                                  float u) {
+  float w[RUN];
+  load_run<RUN>(sh, n, w);
+  if (qrow) {
+    float r[RUN];
+    float s = 0.f;
+#pragma unroll
+    for (int q = 0; q < RUN; ++q) {
+      r[q] = 0.f;
+      if (w[q] > 0.f)
+        r[q] = fmaxf(w[q] / dp.kept - prob_at(qrow, run_index<RUN>(sh, q), it, dq), 0.f);
+      s += r[q];
+    }
+    const float tot = wave_sum(s);
+    if (tot > 0.f) return sh.ci[cand_slot(run_draw<RUN>(r, u * tot))];
+  }
+  return sh.ci[cand_slot(run_draw<RUN>(w, u * dp.kept))];
+}
+
 // Verification: one block per sequence. Rows' parameters come from
 // row_params_kernel; weights are recomputed from the logits as needed (the
-// rows stay in L2), so no per-thread arrays are held.
-template <int EPT>
+// rows stay in L2). The draw after a rejection (or after the last draft) runs
+// over the verifier row's kept tokens, which hold all of max(0, p - q).
+template <int EPT, bool GREEDY>
 __global__ __launch_bounds__(kRowThreads) void verify_kernel(VerifyArgs a) {
   __shared__ RowShared sh;
   const int64_t b = blockIdx.x;
@@ -570,10 +980,11 @@ __global__ __launch_bounds__(kRowThreads) void verify_kernel(VerifyArgs a) {
   const float it = a.inv_temp;
   int k = 0;
   int next = 0;
+#pragma nounroll
   for (; k < G; ++k) {
     const int x = a.draft_tokens[(int64_t)k * a.batch + b];
     const float* trow = a.target_logits + (b * (G + 1) + k) * a.V;
-    if (a.greedy) {
+    if (GREEDY) {
       const int best = row_argmax<EPT>(trow, V, sh);
       if (best != x) {
         next = best;
@@ -589,8 +1000,15 @@ __global__ __launch_bounds__(kRowThreads) void verify_kernel(VerifyArgs a) {
     const float px = in ? prob_at(trow, x, it, dp) : 0.f;
     if (a.u_accept[(int64_t)k * a.batch + b] * qx < px) continue;
     // rejected: draw from max(0, p - q)
+    const int n = compact_kept<EPT>(trow, V, it, dp, sh);
+    if (n <= kMaxCand) {
+      if (threadIdx.x >= 64) return;
+      next = n <= kSmallCand ? list_residual_draw<4>(sh, n, dp, drow, dq, it, a.u_sample[b])
+                         : list_residual_draw<kRunMax>(sh, n, dp, drow, dq, it, a.u_sample[b]);
+      break;
+    }
     auto res = [&](int i) {
-      const int v = threadIdx.x + kRowThreads * i;
+      const int v = elem_v<EPT>(i);
       if (v >= V) return 0.f;
       return fmaxf(prob_at(trow, v, it, dp) - prob_at(drow, v, it, dq), 0.f);
     };
@@ -603,7 +1021,7 @@ __global__ __launch_bounds__(kRowThreads) void verify_kernel(VerifyArgs a) {
       if (v < 0) {
         int last = -1;
         for (int i = 0; i < EPT; ++i)
-          if (res(i) > 0.f) last = threadIdx.x + kRowThreads * i;
+          if (res(i) > 0.f) last = elem_v<EPT>(i);
         float lv = (float)last;
         block_argmax(lv, last, sh);
         v = last;
@@ -618,11 +1036,19 @@ __global__ __launch_bounds__(kRowThreads) void verify_kernel(VerifyArgs a) {
   }
   if (k == G) {  // every draft kept: one more token from the verifier
     const float* trow = a.target_logits + (b * (G + 1) + G) * a.V;
-    if (a.greedy) {
+    if (GREEDY) {
       next = row_argmax<EPT>(trow, V, sh);
     } else {
       const RowDist dp = a.params[a.batch * G + b * (G + 1) + G];
-      next = draw_kept<EPT>(trow, V, it, dp, a.u_sample[b], sh);
+      const int n = compact_kept<EPT>(trow, V, it, dp, sh);
+      if (n <= kMaxCand) {
+        if (threadIdx.x >= 64) return;
+        next = n <= kSmallCand ? list_residual_draw<4>(sh, n, dp, nullptr, dp, it, a.u_sample[b])
+                           : list_residual_draw<kRunMax>(sh, n, dp, nullptr, dp, it,
+                                                         a.u_sample[b]);
+      } else {
+        next = draw_kept<EPT>(trow, V, it, dp, a.u_sample[b], sh);
+      }
     }
   }
   if (threadIdx.x == 0) {
@@ -681,13 +1107,21 @@ hipError_t launch_row_params(const RowParamArgs& a, int ept, hipStream_t stream)
   return hipGetLastError();
 }
 
-hipError_t launch_verify(const VerifyArgs& a, int ept, hipStream_t stream) {
+template <int EPT>
+static void launch_verify_ept(const VerifyArgs& a, hipStream_t stream) {
   const dim3 grid((unsigned)a.batch);
+  if (a.greedy)
+    hipLaunchKernelGGL((verify_kernel<EPT, true>), grid, dim3(kRowThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((verify_kernel<EPT, false>), grid, dim3(kRowThreads), 0, stream, a);
+}
+
+hipError_t launch_verify(const VerifyArgs& a, int ept, hipStream_t stream) {
   switch (ept) {
-    case 16: hipLaunchKernelGGL(verify_kernel<16>, grid, dim3(kRowThreads), 0, stream, a); break;
-    case 32: hipLaunchKernelGGL(verify_kernel<32>, grid, dim3(kRowThreads), 0, stream, a); break;
-    case 48: hipLaunchKernelGGL(verify_kernel<48>, grid, dim3(kRowThreads), 0, stream, a); break;
-    case 64: hipLaunchKernelGGL(verify_kernel<64>, grid, dim3(kRowThreads), 0, stream, a); break;
+    case 16: launch_verify_ept<16>(a, stream); break;
+    case 32: launch_verify_ept<32>(a, stream); break;
+    case 48: launch_verify_ept<48>(a, stream); break;
+    case 64: launch_verify_ept<64>(a, stream); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
