@@ -343,48 +343,83 @@ def main_decode(args):
     samp = B.make_sampling(V, wl.temperature, wl.top_p)
     od = x["o_draft"].reshape(G, Bt, -1)
     cats = ["draft_head", "sample", "verify_head", "verify"]
-    ev = {c: [] for c in cats}
 
-    def mark(c, fn, timed):
-        if not timed:
-            fn()
-            return
-        a = torch.cuda.Event(enable_timing=True)
-        b = torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        fn()
-        b.record(stream)
-        ev[c].append((a, b))
+    def run(cat, st):
+        """The library calls of one kernel category of a step, on stream handle st."""
+        if cat == "draft_head":
+            for k in range(G):
+                B.head_logits(Bt, V, wl.d_draft, B.MLS_BF16, od[k].data_ptr(),
+                              x["W_draft"].data_ptr(), ldk[k].data_ptr(), st)
+        elif cat == "sample":
+            for k in range(G):
+                B.sample(samp, Bt, ldk[k].data_ptr(), x["u_draft"][k].data_ptr(),
+                         tok[k].data_ptr(), st)
+        elif cat == "verify_head":
+            B.head_logits(Bt * (G + 1), V, wl.d_target, B.MLS_BF16, x["o_target"].data_ptr(),
+                          x["W_target"].data_ptr(), lt.data_ptr(), st)
+        else:
+            B.spec_verify(samp, Bt, G, ldk.data_ptr(), lt.data_ptr(), tok.data_ptr(),
+                          u_acc.data_ptr(), x["u_sample"].data_ptr(), n_acc.data_ptr(),
+                          nxt.data_ptr(), ws.data_ptr(), ws_b, st)
 
-    def step(timed=False):
+    def step(st):
         for k in range(G):
-            mark("draft_head", lambda: B.head_logits(Bt, V, wl.d_draft, B.MLS_BF16, od[k].data_ptr(),
-                                                     x["W_draft"].data_ptr(), ldk[k].data_ptr(), sh),
-                 timed)
-            mark("sample", lambda: B.sample(samp, Bt, ldk[k].data_ptr(), x["u_draft"][k].data_ptr(),
-                                            tok[k].data_ptr(), sh), timed)
-        mark("verify_head", lambda: B.head_logits(Bt * (G + 1), V, wl.d_target, B.MLS_BF16,
-                                                  x["o_target"].data_ptr(), x["W_target"].data_ptr(),
-                                                  lt.data_ptr(), sh), timed)
-        mark("verify", lambda: B.spec_verify(samp, Bt, G, ldk.data_ptr(), lt.data_ptr(),
-                                             tok.data_ptr(), u_acc.data_ptr(),
-                                             x["u_sample"].data_ptr(), n_acc.data_ptr(),
-                                             nxt.data_ptr(), ws.data_ptr(), ws_b, sh), timed)
+            B.head_logits(Bt, V, wl.d_draft, B.MLS_BF16, od[k].data_ptr(),
+                          x["W_draft"].data_ptr(), ldk[k].data_ptr(), st)
+            B.sample(samp, Bt, ldk[k].data_ptr(), x["u_draft"][k].data_ptr(),
+                     tok[k].data_ptr(), st)
+        run("verify_head", st)
+        run("verify", st)
+
+    def capture(fn):
+        """One call of fn captured as a HIP graph (after a run on the capture stream)."""
+        side = torch.cuda.Stream(device=dev)
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            fn(side.cuda_stream)
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn(torch.cuda.current_stream(dev).cuda_stream)
+        torch.cuda.synchronize()
+        return g
+
+    def timed(fn, n):
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(n):
+            fn()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / n
 
     for _ in range(args.warmup):
-        step()
+        step(sh)
     torch.cuda.synchronize()
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    t0.record(stream)
-    for _ in range(args.steps):
-        step(timed=True)
-    t1.record(stream)
+    eager_out = [t.clone() for t in (tok, n_acc, nxt)]
+    eager_ms = timed(lambda: step(sh), args.steps)
+    # The step is launch-bound when each library call is issued from Python, so
+    # the timed region replays a HIP graph of one step: the same kernels on the
+    # same buffers, without host launch gaps.
+    g_step = capture(step)
+    g_cat = {c: capture(lambda st, c=c: run(c, st)) for c in cats}
+    for t in (tok, n_acc, nxt):
+        t.fill_(-7)
+    g_step.replay()
     torch.cuda.synchronize()
-    ms_step = t0.elapsed_time(t1) / args.steps
-    per = {c: sum(a.elapsed_time(b) for a, b in ev[c]) / args.steps for c in cats}
+    replay_ok = all(torch.equal(a, b) for a, b in zip(eager_out, (tok, n_acc, nxt)))
+    for _ in range(args.warmup):
+        g_step.replay()
+    ms_step = timed(g_step.replay, args.steps)
+    per = {c: timed(g_cat[c].replay, args.steps) for c in cats}
+    replay_ok = replay_ok and all(torch.equal(a, b) for a, b in zip(eager_out, (tok, n_acc, nxt)))
+    if not replay_ok:
+        raise SystemExit("graph replay outputs differ from the eager step")
     rows = Bt * G + Bt * (G + 1)
-    log(f"{ms_step:.3f} ms/step, mean accepted {n_acc.float().mean().item():.2f} of {G}")
+    log(f"{ms_step:.3f} ms/step (graph replay; eager launches {eager_ms:.3f} ms/step), "
+        f"mean accepted {n_acc.float().mean().item():.2f} of {G}")
     for c in cats:
         log(f"  {c:12s} {per[c]:8.4f} ms/step")
     # algorithmic work per step of each kernel category
@@ -430,6 +465,9 @@ def main_decode(args):
                    "d_verifier": dt_, "temperature": wl.temperature, "top_p": wl.top_p,
                    "parallelism": "single GPU"},
         "mean_accepted": n_acc.float().mean().item(),
+        "launch": "one step captured as a HIP graph and replayed (outputs checked against "
+                  "the eager step)",
+        "eager_ms_per_step": eager_ms,
         "roofline": {"bound": bound, "kernel": dom, "achieved": achieved / scale,
                      "peak": peak / scale, "unit": unit, "frac": achieved / peak,
                      "traffic": profiled_traffic(name, dom, "decode")},

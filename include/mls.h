@@ -99,8 +99,10 @@ enum mls_device_flags {
  *   tau           distillation temperature, finite and > 0 (1 = eq. (2) as printed)
  *   in_dtype      an mls_dtype
  *   flags         OR of mls_flags
- *   vocab_chunk   backward vocabulary chunk width (0 = chosen by the library);
- *                 rounded up to a multiple of 256
+ *   vocab_chunk   backward vocabulary chunk width, rounded up to a multiple of
+ *                 256; 0 = chosen by the library: at least four balanced
+ *                 chunks (more if one chunk's bf16 logit-gradient slabs would
+ *                 pass 4 GiB), so no slab spans the whole vocabulary
  */
 typedef struct mls_problem {
   int32_t M;

@@ -83,6 +83,7 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 constexpr int64_t kSlabTargetBytes = 4ll << 30;  // logit-gradient slab(s) per chunk
+constexpr int64_t kMinChunks = 4;                 // the default plan never holds a [T, V] slab
 
 struct Plan {
   int M = 0;
@@ -159,9 +160,14 @@ void make_plan(const mls_problem* p, Plan& pl) {
   if (p->vocab_chunk > 0) {
     vc = round_up(p->vocab_chunk, 256);
   } else {
-    // the wide path keeps one slab layout, the general path two
-    vc = kSlabTargetBytes / ((pl.wide ? 1ll : 2ll) * pl.M * pl.T_pad * pl.es);
-    vc = vc / 256 * 256;
+    // At least kMinChunks balanced chunks, more when the slabs of one chunk
+    // would exceed kSlabTargetBytes (the wide path keeps one slab layout, the
+    // general path two), so the logit-gradient slab never spans the whole
+    // vocabulary (V > 256).
+    const int64_t per_row = (pl.wide ? 1ll : 2ll) * pl.M * pl.T_pad * pl.es;
+    const int64_t fit = std::max<int64_t>(256, kSlabTargetBytes / per_row / 256 * 256);
+    const int64_t n = std::max<int64_t>(kMinChunks, (p->V + fit - 1) / fit);
+    vc = round_up((p->V + n - 1) / n, 256);
   }
   pl.Vc = std::max<int64_t>(256, std::min(vc, vmax));
   pl.n_chunks = (int)((p->V + pl.Vc - 1) / pl.Vc);

@@ -88,6 +88,11 @@ def test_query_sizes_reports_workspace_and_stats():
     M, T = 3, 4096
     assert st >= (4 * M * T + T) * 4 + 8
     assert ws >= M * ((50304 + 127) // 128) * T * 16  # forward partial rows
+    # the default backward plan splits the vocabulary (>= 4 chunks): its bf16
+    # logit-gradient slab is far below a full [T, V] slab per sub-model
+    assert ws < M * T * 50304 * 2 // 2
+    p1 = _fake_problem(vocab_chunk=50304)  # an explicit single chunk is the caller's choice
+    assert B.query_sizes(p1)[0] >= M * T * 50304 * 2
 
 
 @pytest.mark.parametrize("field,value,status", [

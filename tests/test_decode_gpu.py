@@ -110,6 +110,27 @@ def test_sample_parity(case):
     assert np.array_equal(greedy, _np(logits).argmax(axis=1))
 
 
+# (logit scale, top_p) at V = 49152, temperature 1: with N(0, scale^2) logits
+# these send rows down each threshold-search path (nucleus sizes from most of
+# the vocabulary down to one token): whole-row search, bound rounds over the
+# row ending in a small or a larger final list, first-list rounds ending in a
+# small or a larger final list.
+SCALE_CASES = [(0.01, 0.9), (1.2, 0.5), (2.0, 0.5), (3.0, 0.5), (3.0, 0.7), (4.0, 0.9),
+               (4.0, 0.95), (4.0, 0.97), (5.0, 0.99), (8.0, 0.99)]
+
+
+@pytest.mark.parametrize("scale,top_p", SCALE_CASES, ids=[f"s{c[0]}_p{c[1]}" for c in SCALE_CASES])
+def test_sample_across_logit_scales(scale, top_p):
+    rows, V = 24, 49152
+    print(f"[decode] sample scale={scale} p={top_p}", flush=True)
+    g = torch.Generator(device=DEV).manual_seed(int(scale * 100) + int(top_p * 1000))
+    logits = torch.randn(rows, V, generator=g, device=DEV) * scale
+    u = torch.rand(rows, generator=g, device=DEV)
+    tok = _np(D.sample(logits, u, temperature=1.0, top_p=top_p)).astype(np.int64)
+    _check_samples(_np(logits).astype(np.float64), _np(u).astype(np.float64), tok, 1.0, top_p,
+                   max_ambiguous=0.05)
+
+
 def test_sample_ties_and_extreme_uniforms():
     """Exactly tied logits straddling the nucleus boundary (lower indices kept
     first), and uniforms at 0 and just below 1."""
@@ -173,7 +194,9 @@ def _verify_inputs(B, G, V, d_t, d_d, seed):
 
 @pytest.mark.parametrize("B,G,V,temp,top_p", [(16, 4, 3000, 0.4, 0.9), (24, 6, 49152, 0.4, 0.9),
                                                (10, 3, 1000, 1.0, 1.0), (8, 0, 5000, 0.4, 0.9),
-                                               (12, 5, 777, 0.8, 0.6)])
+                                               (12, 5, 777, 0.8, 0.6),
+                                               # kept sets beyond the list capacity: whole-row draws
+                                               (12, 3, 5000, 1.0, 1.0)])
 def test_verify_parity(B, G, V, temp, top_p):
     print(f"[decode] verify B={B} gamma={G} V={V} T={temp} p={top_p}", flush=True)
     wl, x, dl, tl = _verify_inputs(B, G, V, 256, 128, seed=B * 31 + G)
@@ -320,3 +343,49 @@ def test_verify_single_token_nuclei_accept_agreeing_drafts():
     assert _np(x).tolist() == _np(top[:, G]).tolist()
     p = D.sample(tl[:, 0].contiguous(), us, temperature=0.4, top_p=0.9)
     assert _np(p).tolist() == _np(top[:, 0]).tolist()
+
+
+def test_graph_replay_matches_eager():
+    """Sampling and verification captured in a HIP graph: each replay, with
+    eager work and synchronisations between replays, gives the eager result."""
+    from paper_2608_09703_amd import binding as B
+    Bt, G, V = 16, 4, 49152
+    print(f"[decode] graph replay B={Bt} gamma={G} V={V}", flush=True)
+    wl, x, dl, tl = _verify_inputs(Bt, G, V, 256, 128, seed=41)
+    dls = dl.transpose(0, 1).contiguous()                  # [gamma][batch][V]
+    tls = tl.contiguous()
+    ud, ua, us = x["u_draft"].contiguous(), x["u_accept"].t().contiguous(), x["u_sample"]
+    tok = torch.empty(G, Bt, dtype=torch.int32, device=DEV)
+    n_acc = torch.empty(Bt, dtype=torch.int32, device=DEV)
+    nxt = torch.empty(Bt, dtype=torch.int32, device=DEV)
+    ws_b = B.spec_verify_workspace(Bt, G)
+    ws = torch.empty(ws_b, dtype=torch.uint8, device=DEV)
+    samp = B.make_sampling(V, 0.4, 0.9)
+
+    def step(st):
+        for k in range(G):
+            B.sample(samp, Bt, dls[k].data_ptr(), ud[k].data_ptr(), tok[k].data_ptr(), st)
+        B.spec_verify(samp, Bt, G, dls.data_ptr(), tls.data_ptr(), tok.data_ptr(), ua.data_ptr(),
+                      us.data_ptr(), n_acc.data_ptr(), nxt.data_ptr(), ws.data_ptr(), ws_b, st)
+
+    step(torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in (tok, n_acc, nxt)]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step(side.cuda_stream)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step(torch.cuda.current_stream().cuda_stream)
+    other = torch.randn(8, V, device=DEV)
+    for rep in range(3):
+        for t in (tok, n_acc, nxt):
+            t.fill_(-3)
+        g.replay()
+        torch.cuda.synchronize()
+        assert all(torch.equal(a, b) for a, b in zip(ref, (tok, n_acc, nxt))), f"replay {rep}"
+        D.sample(other, torch.rand(8, device=DEV), temperature=0.7, top_p=0.8)  # eager work
+        torch.cuda.synchronize()
