@@ -342,6 +342,9 @@ def main_decode(args):
     ws = torch.empty(ws_b, dtype=torch.uint8, device=dev)
     samp = B.make_sampling(V, wl.temperature, wl.top_p)
     od = x["o_draft"].reshape(G, Bt, -1)
+    # the draft rows' distribution records, kept by the sampler for the verification
+    dpar = torch.empty(max(G, 1) * Bt * B.ROW_PARAMS_BYTES, dtype=torch.uint8, device=dev)
+    dpar_k = [dpar.data_ptr() + k * Bt * B.ROW_PARAMS_BYTES for k in range(G)]
     cats = ["draft_head", "sample", "verify_head", "verify"]
 
     def run(cat, st):
@@ -353,21 +356,21 @@ def main_decode(args):
         elif cat == "sample":
             for k in range(G):
                 B.sample(samp, Bt, ldk[k].data_ptr(), x["u_draft"][k].data_ptr(),
-                         tok[k].data_ptr(), st)
+                         tok[k].data_ptr(), st, params=dpar_k[k])
         elif cat == "verify_head":
             B.head_logits(Bt * (G + 1), V, wl.d_target, B.MLS_BF16, x["o_target"].data_ptr(),
                           x["W_target"].data_ptr(), lt.data_ptr(), st)
         else:
             B.spec_verify(samp, Bt, G, ldk.data_ptr(), lt.data_ptr(), tok.data_ptr(),
                           u_acc.data_ptr(), x["u_sample"].data_ptr(), n_acc.data_ptr(),
-                          nxt.data_ptr(), ws.data_ptr(), ws_b, st)
+                          nxt.data_ptr(), ws.data_ptr(), ws_b, st, draft_params=dpar.data_ptr())
 
     def step(st):
         for k in range(G):
             B.head_logits(Bt, V, wl.d_draft, B.MLS_BF16, od[k].data_ptr(),
                           x["W_draft"].data_ptr(), ldk[k].data_ptr(), st)
             B.sample(samp, Bt, ldk[k].data_ptr(), x["u_draft"][k].data_ptr(),
-                     tok[k].data_ptr(), st)
+                     tok[k].data_ptr(), st, params=dpar_k[k])
         run("verify_head", st)
         run("verify", st)
 

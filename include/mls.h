@@ -269,14 +269,22 @@ typedef struct mls_sampling {
 mls_status mls_head_logits(int64_t T, int64_t V, int64_t d, int32_t dtype, const void* o,
                            const void* W, float* logits, void* stream);
 
+/* Bytes of one row's sampling-distribution record (an opaque device record:
+ * the row's maximum, total and kept mass, nucleus threshold and tie cut). */
+#define MLS_ROW_PARAMS_BYTES 20
+
 /*
  * tokens[r] (int32, device) = a draw from row r of logits [rows][V] with
- * uniform u[r] (device [rows]; may be NULL when greedy).
+ * uniform u[r] (device [rows]; may be NULL when greedy). When params is not
+ * NULL (and not greedy), row r's distribution record is also written to
+ * params + r * MLS_ROW_PARAMS_BYTES (device, 4-byte aligned): a drafting loop
+ * can hand these records to mls_spec_verify as draft_params.
  */
 mls_status mls_sample(const mls_sampling* s, int64_t rows, const float* logits, const float* u,
-                      int32_t* tokens, void* stream);
+                      int32_t* tokens, void* params, void* stream);
 
-/* Workspace bytes of mls_spec_verify for a batch and draft length. */
+/* Workspace bytes of mls_spec_verify for a batch and draft length (enough
+ * with or without draft_params). */
 mls_status mls_spec_verify_workspace(int64_t batch, int64_t gamma, size_t* bytes);
 
 /*
@@ -296,13 +304,17 @@ mls_status mls_spec_verify_workspace(int64_t batch, int64_t gamma, size_t* bytes
  * next_token is drawn from the verifier's distribution at position gamma.
  * Greedy mode keeps a token while it equals the verifier's argmax and emits
  * the verifier's argmax (u_accept, u_sample and the workspace may be NULL).
+ * draft_params (device, may be NULL): [gamma][batch] records of
+ * MLS_ROW_PARAMS_BYTES from mls_sample on the same draft rows with the same
+ * sampling settings; then the draft rows' distributions are not recomputed.
  * Outputs n_accepted, next_token: int32 [batch]. Asynchronous on stream.
  */
 mls_status mls_spec_verify(const mls_sampling* s, int64_t batch, int64_t gamma,
                            const float* draft_logits, const float* target_logits,
                            const int32_t* draft_tokens, const float* u_accept,
-                           const float* u_sample, int32_t* n_accepted, int32_t* next_token,
-                           void* workspace, size_t workspace_bytes, void* stream);
+                           const float* u_sample, const void* draft_params,
+                           int32_t* n_accepted, int32_t* next_token, void* workspace,
+                           size_t workspace_bytes, void* stream);
 
 /*
  * Host helper: loss coefficients of the objective (host arrays of length M).

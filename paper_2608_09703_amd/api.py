@@ -260,28 +260,39 @@ def _sampling(V, temperature, top_p, greedy):
 
 
 def sample(logits: torch.Tensor, u: Optional[torch.Tensor], *, temperature: float = 1.0,
-           top_p: float = 1.0, greedy: bool = False) -> torch.Tensor:
-    """int32 tokens, one per row of ``logits [rows, V]`` (fp32), with uniforms ``u [rows]``."""
+           top_p: float = 1.0, greedy: bool = False,
+           params: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """int32 tokens, one per row of ``logits [rows, V]`` (fp32), with uniforms ``u [rows]``.
+
+    ``params``: optional uint8 tensor of ``rows * ROW_PARAMS_BYTES`` bytes that
+    receives the rows' distribution records (for ``spec_verify(draft_params=)``).
+    """
     if logits.dtype != torch.float32 or not logits.is_contiguous() or logits.dim() != 2:
         raise ValueError("logits must be a contiguous float32 [rows, V] tensor")
     rows, V = logits.shape
     if u is not None and (u.dtype != torch.float32 or u.shape != (rows,) or not u.is_contiguous()):
         raise ValueError("u must be a contiguous float32 [rows] tensor")
+    if params is not None and (params.dtype != torch.uint8 or not params.is_contiguous() or
+                               params.numel() < rows * B.ROW_PARAMS_BYTES):
+        raise ValueError("params must be a contiguous uint8 tensor of rows * ROW_PARAMS_BYTES")
     tok = torch.empty(rows, dtype=torch.int32, device=logits.device)
     B.sample(_sampling(V, temperature, top_p, greedy), rows, logits.data_ptr(),
-             u.data_ptr() if u is not None else None, tok.data_ptr(), _stream(logits.device))
+             u.data_ptr() if u is not None else None, tok.data_ptr(), _stream(logits.device),
+             params.data_ptr() if params is not None else None)
     return tok
 
 
 def spec_verify(draft_logits: Optional[torch.Tensor], target_logits: torch.Tensor,
                 draft_tokens: Optional[torch.Tensor], u_accept: Optional[torch.Tensor],
                 u_sample: Optional[torch.Tensor], *, temperature: float = 1.0, top_p: float = 1.0,
-                greedy: bool = False):
+                greedy: bool = False, draft_params: Optional[torch.Tensor] = None):
     """``(n_accepted [B], next_token [B])`` (int32) of speculative verification.
 
     Draft-side arrays in drafting order: ``draft_logits [gamma, B, V]`` (fp32),
     ``draft_tokens [gamma, B]`` (int32), ``u_accept [gamma, B]``; verifier side
     ``target_logits [B, gamma + 1, V]`` (fp32) and ``u_sample [B]``.
+    ``draft_params``: optional uint8 records ``[gamma, B]`` from ``sample(params=)``
+    on the draft rows with the same settings (then not recomputed).
     """
     Bt, G1, V = target_logits.shape
     G = G1 - 1
@@ -302,9 +313,14 @@ def spec_verify(draft_logits: Optional[torch.Tensor], target_logits: torch.Tenso
     ws_bytes = 0 if greedy else B.spec_verify_workspace(Bt, G)
     ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev) if not greedy else None
     ptr = (lambda x: x.data_ptr() if x is not None else None)
+    if draft_params is not None and (draft_params.dtype != torch.uint8 or
+                                     not draft_params.is_contiguous() or
+                                     draft_params.numel() < G * Bt * B.ROW_PARAMS_BYTES):
+        raise ValueError("draft_params must be contiguous uint8 of gamma * B records")
     B.spec_verify(_sampling(V, temperature, top_p, greedy), Bt, G, ptr(draft_logits),
                   target_logits.data_ptr(), ptr(draft_tokens), ptr(u_accept), ptr(u_sample),
-                  n_acc.data_ptr(), nxt.data_ptr(), ptr(ws), ws_bytes, _stream(dev))
+                  n_acc.data_ptr(), nxt.data_ptr(), ptr(ws), ws_bytes, _stream(dev),
+                  draft_params=ptr(draft_params))
     return n_acc, nxt
 
 

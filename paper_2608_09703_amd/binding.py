@@ -136,11 +136,11 @@ def lib():
         S = ctypes.POINTER(Sampling)
         L.mls_head_logits.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
                                       vp, vp, vp, vp]
-        L.mls_sample.argtypes = [S, ctypes.c_int64, vp, vp, vp, vp]
+        L.mls_sample.argtypes = [S, ctypes.c_int64, vp, vp, vp, vp, vp]
         L.mls_spec_verify_workspace.argtypes = [ctypes.c_int64, ctypes.c_int64,
                                                 ctypes.POINTER(ctypes.c_size_t)]
         L.mls_spec_verify.argtypes = [S, ctypes.c_int64, ctypes.c_int64, vp, vp, vp, vp, vp, vp, vp,
-                                      vp, ctypes.c_size_t, vp]
+                                      vp, vp, ctypes.c_size_t, vp]
         L.mls_coeffs.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_float, ctypes.c_float,
                                  ctypes.c_int32, fp, fp, fp]
         L.mls_read_stats_header.argtypes = [P, vp, vp, ctypes.POINTER(ctypes.c_int32),
@@ -248,8 +248,12 @@ def head_logits(T: int, V: int, d: int, dtype: int, o: int, W: int, logits: int,
     check(lib().mls_head_logits(T, V, d, dtype, o, W, logits, stream), "mls_head_logits")
 
 
-def sample(s: Sampling, rows: int, logits: int, u: Optional[int], tokens: int, stream: int):
-    check(lib().mls_sample(ctypes.byref(s), rows, logits, u, tokens, stream), "mls_sample")
+ROW_PARAMS_BYTES = 20  # MLS_ROW_PARAMS_BYTES
+
+
+def sample(s: Sampling, rows: int, logits: int, u: Optional[int], tokens: int, stream: int,
+           params: Optional[int] = None):
+    check(lib().mls_sample(ctypes.byref(s), rows, logits, u, tokens, params, stream), "mls_sample")
 
 
 def spec_verify_workspace(batch: int, gamma: int) -> int:
@@ -261,10 +265,10 @@ def spec_verify_workspace(batch: int, gamma: int) -> int:
 def spec_verify(s: Sampling, batch: int, gamma: int, draft_logits: Optional[int],
                 target_logits: int, draft_tokens: Optional[int], u_accept: Optional[int],
                 u_sample: Optional[int], n_accepted: int, next_token: int, ws: Optional[int],
-                ws_bytes: int, stream: int):
+                ws_bytes: int, stream: int, draft_params: Optional[int] = None):
     check(lib().mls_spec_verify(ctypes.byref(s), batch, gamma, draft_logits, target_logits,
-                                draft_tokens, u_accept, u_sample, n_accepted, next_token, ws,
-                                ws_bytes, stream), "mls_spec_verify")
+                                draft_tokens, u_accept, u_sample, draft_params, n_accepted,
+                                next_token, ws, ws_bytes, stream), "mls_spec_verify")
 
 
 def coeffs(M: int, teacher: int = -1, alpha: float = 0.0, tau: float = 1.0,

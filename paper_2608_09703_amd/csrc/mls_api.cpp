@@ -791,15 +791,17 @@ mls_status mls_head_logits(int64_t T, int64_t V, int64_t d, int32_t dtype, const
   return MLS_OK;
 }
 
+static_assert(sizeof(RowDist) == MLS_ROW_PARAMS_BYTES, "row parameter record size");
+
 mls_status mls_sample(const mls_sampling* s, int64_t rows, const float* logits, const float* u,
-                      int32_t* tokens, void* stream) {
+                      int32_t* tokens, void* params, void* stream) {
   g_last_error.clear();
   mls_status st = validate_sampling(s);
   if (st != MLS_OK) return st;
   if (rows < 1 || rows > (1ll << 31) - 1) return fail(MLS_INVALID_ARG, "rows=%lld out of range", (long long)rows);
   if (!logits || !tokens || (!s->greedy && !u))
     return fail(MLS_INVALID_ARG, "logits, tokens and (unless greedy) u must be non-NULL");
-  if (!aligned(logits, 4) || !aligned(u, 4) || !aligned(tokens, 4))
+  if (!aligned(logits, 4) || !aligned(u, 4) || !aligned(tokens, 4) || !aligned(params, 4))
     return fail(MLS_INVALID_ARG, "misaligned pointer");
   SampleArgs a;
   memset(&a, 0, sizeof(a));
@@ -811,6 +813,7 @@ mls_status mls_sample(const mls_sampling* s, int64_t rows, const float* logits, 
   a.logits = logits;
   a.u = u;
   a.tokens = tokens;
+  a.params = s->greedy ? nullptr : static_cast<RowDist*>(params);
   hipStream_t hs = static_cast<hipStream_t>(stream);
   hipError_t e;
   {
@@ -833,8 +836,9 @@ mls_status mls_spec_verify_workspace(int64_t batch, int64_t gamma, size_t* bytes
 mls_status mls_spec_verify(const mls_sampling* s, int64_t batch, int64_t gamma,
                            const float* draft_logits, const float* target_logits,
                            const int32_t* draft_tokens, const float* u_accept,
-                           const float* u_sample, int32_t* n_accepted, int32_t* next_token,
-                           void* workspace, size_t workspace_bytes, void* stream) {
+                           const float* u_sample, const void* draft_params,
+                           int32_t* n_accepted, int32_t* next_token, void* workspace,
+                           size_t workspace_bytes, void* stream) {
   g_last_error.clear();
   mls_status st = validate_sampling(s);
   if (st != MLS_OK) return st;
@@ -848,23 +852,26 @@ mls_status mls_spec_verify(const mls_sampling* s, int64_t batch, int64_t gamma,
   if (!s->greedy && workspace_bytes < verify_ws_bytes(batch, gamma))
     return fail(MLS_WORKSPACE_TOO_SMALL, "verification needs %zu workspace bytes, got %zu",
                 verify_ws_bytes(batch, gamma), workspace_bytes);
-  if (!aligned(workspace, 16)) return fail(MLS_INVALID_ARG, "misaligned workspace");
+  if (!aligned(workspace, 16) || !aligned(draft_params, 4))
+    return fail(MLS_INVALID_ARG, "misaligned workspace or draft_params");
   hipStream_t hs = static_cast<hipStream_t>(stream);
   const int ept = row_elems_per_thread(s->V);
   const float inv_temp = s->greedy ? 1.f : 1.f / s->temperature;
   hipError_t e;
+  // workspace: draft rows' records [gamma][batch], then the verifier rows' [batch][gamma + 1]
   RowDist* params = static_cast<RowDist*>(workspace);
+  const bool have_draft = draft_params != nullptr && gamma > 0;
   if (!s->greedy) {
     RowParamArgs r;
     memset(&r, 0, sizeof(r));
-    r.rows0 = batch * gamma;
+    r.rows0 = have_draft ? 0 : batch * gamma;
     r.rows1 = batch * (gamma + 1);
     r.V = s->V;
     r.inv_temp = inv_temp;
     r.top_p = s->top_p;
     r.logits0 = draft_logits;
     r.logits1 = target_logits;
-    r.params = params;
+    r.params = have_draft ? params + batch * gamma : params;
     {
       ProfScope ps("row_params", hs);
       e = launch_row_params(r, ept, hs);
@@ -873,7 +880,8 @@ mls_status mls_spec_verify(const mls_sampling* s, int64_t batch, int64_t gamma,
   }
   VerifyArgs a;
   memset(&a, 0, sizeof(a));
-  a.params = params;
+  a.dparams = have_draft ? static_cast<const RowDist*>(draft_params) : params;
+  a.tparams = params + batch * gamma;
   a.batch = batch;
   a.V = s->V;
   a.gamma = (int32_t)gamma;

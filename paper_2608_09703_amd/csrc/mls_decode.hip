@@ -864,6 +864,7 @@ __global__ __launch_bounds__(kRowThreads) void sample_kernel(SampleArgs a) {
     } else {
       tok = row_draw<EPT>(e, d, a.u[r], sh);
     }
+    if (threadIdx.x == 0 && a.params) a.params[r] = d;
   }
   if (threadIdx.x == 0) a.tokens[r] = tok;
 }
@@ -993,8 +994,8 @@ __global__ __launch_bounds__(kRowThreads) void verify_kernel(VerifyArgs a) {
       continue;
     }
     const float* drow = a.draft_logits + ((int64_t)k * a.batch + b) * a.V;
-    const RowDist dq = a.params[(int64_t)k * a.batch + b];
-    const RowDist dp = a.params[a.batch * G + b * (G + 1) + k];
+    const RowDist dq = a.dparams[(int64_t)k * a.batch + b];
+    const RowDist dp = a.tparams[b * (G + 1) + k];
     const bool in = x >= 0 && x < V;
     const float qx = in ? prob_at(drow, x, it, dq) : 0.f;
     const float px = in ? prob_at(trow, x, it, dp) : 0.f;
@@ -1039,7 +1040,7 @@ __global__ __launch_bounds__(kRowThreads) void verify_kernel(VerifyArgs a) {
     if (GREEDY) {
       next = row_argmax<EPT>(trow, V, sh);
     } else {
-      const RowDist dp = a.params[a.batch * G + b * (G + 1) + G];
+      const RowDist dp = a.tparams[b * (G + 1) + G];
       const int n = compact_kept<EPT>(trow, V, it, dp, sh);
       if (n <= kMaxCand) {
         if (threadIdx.x >= 64) return;

@@ -184,6 +184,14 @@ struct HeadArgs {
   int32_t n_vt;
   int32_t group_v;
 };
+// Parameters of one row's sampling distribution.
+struct RowDist {
+  float m;      // max logit / temperature
+  float total;  // sum of exp weights exp(l / temperature - m)
+  float theta;  // nucleus threshold on the exp weight (0: keep every positive weight)
+  int tie_cut;  // tokens with weight == theta are kept for index <= tie_cut
+  float kept;   // sum of kept weights
+};
 struct SampleArgs {
   int64_t rows;
   int64_t V;
@@ -193,14 +201,7 @@ struct SampleArgs {
   const float* logits;  // [rows][V]
   const float* u;       // [rows]
   int32_t* tokens;      // [rows]
-};
-// Parameters of one row's sampling distribution.
-struct RowDist {
-  float m;      // max logit / temperature
-  float total;  // sum of exp weights exp(l / temperature - m)
-  float theta;  // nucleus threshold on the exp weight (0: keep every positive weight)
-  int tie_cut;  // tokens with weight == theta are kept for index <= tie_cut
-  float kept;   // sum of kept weights
+  RowDist* params;      // [rows] distribution records, or nullptr
 };
 struct RowParamArgs {
   int64_t rows0;          // rows of logits0, then rows1 rows of logits1
@@ -213,7 +214,8 @@ struct RowParamArgs {
   RowDist* params;        // [rows0 + rows1]
 };
 struct VerifyArgs {
-  const RowDist* params;  // draft rows [gamma][batch], then verifier rows [batch][gamma + 1]
+  const RowDist* dparams;  // draft rows [gamma][batch]
+  const RowDist* tparams;  // verifier rows [batch][gamma + 1]
   int64_t batch;
   int64_t V;
   int32_t gamma;

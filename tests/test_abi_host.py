@@ -263,6 +263,15 @@ def test_decode_entry_points_reject_bad_arguments_before_device_work():
     with pytest.raises(B.MlsError) as e:  # sampling without uniforms
         B.sample(s, 4, fake, None, fake + 4096, None)
     assert e.value.status == B.MLS_INVALID_ARG
+    with pytest.raises(B.MlsError) as e:  # misaligned distribution records
+        B.sample(s, 4, fake, fake + 8192, fake + 4096, None, params=fake + 16386)
+    assert e.value.status == B.MLS_INVALID_ARG
+    assert B.ROW_PARAMS_BYTES == 20
+    with pytest.raises(B.MlsError) as e:  # misaligned draft records
+        B.spec_verify(s, 8, 6, fake, fake + (1 << 32), fake + (2 << 32), fake + (3 << 32),
+                      fake + (4 << 32), fake + (5 << 32), fake + (6 << 32), fake + (7 << 32),
+                      B.spec_verify_workspace(8, 6), None, draft_params=fake + (8 << 32) + 2)
+    assert e.value.status == B.MLS_INVALID_ARG
     ws = B.spec_verify_workspace(8, 6)
     assert ws >= (8 * 6 + 8 * 7) * 20
     with pytest.raises(B.MlsError) as e:

@@ -389,3 +389,30 @@ def test_graph_replay_matches_eager():
         assert all(torch.equal(a, b) for a, b in zip(ref, (tok, n_acc, nxt))), f"replay {rep}"
         D.sample(other, torch.rand(8, device=DEV), temperature=0.7, top_p=0.8)  # eager work
         torch.cuda.synchronize()
+
+
+def test_draft_params_from_the_sampler():
+    """Records written by sample(params=) on the draft rows give the same
+    verification as recomputing them, at the paper vocabulary."""
+    Bt, G, V = 24, 5, 49152
+    print(f"[decode] draft params B={Bt} gamma={G} V={V}", flush=True)
+    wl, x, dl, tl = _verify_inputs(Bt, G, V, 256, 128, seed=57)
+    from paper_2608_09703_amd import binding as B
+    dls = dl.transpose(0, 1).contiguous()                   # [gamma][batch][V]
+    rec = torch.zeros(G * Bt * B.ROW_PARAMS_BYTES, dtype=torch.uint8, device=DEV)
+    toks = []
+    for k in range(G):
+        toks.append(D.sample(dls[k], x["u_draft"][k].contiguous(), temperature=0.4, top_p=0.9,
+                             params=rec[k * Bt * B.ROW_PARAMS_BYTES:(k + 1) * Bt * B.ROW_PARAMS_BYTES]))
+        ref_k = D.sample(dls[k], x["u_draft"][k].contiguous(), temperature=0.4, top_p=0.9)
+        assert torch.equal(toks[-1], ref_k)  # writing the records does not change the draw
+    drafts = torch.stack(toks).contiguous()
+    ua, us = x["u_accept"].t().contiguous(), x["u_sample"]
+    a = D.spec_verify(dls, tl, drafts, ua, us, temperature=0.4, top_p=0.9)
+    b = D.spec_verify(dls, tl, drafts, ua, us, temperature=0.4, top_p=0.9, draft_params=rec)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+    # the records hold the draft distribution's maximum and kept mass
+    f = rec.view(torch.float32).view(G, Bt, 5).cpu()
+    z = (dls.float().cpu() * (1 / 0.4)).max(dim=2).values
+    assert torch.allclose(f[:, :, 0], z, rtol=1e-6)
+    assert bool(((f[:, :, 4] > 0) & (f[:, :, 4] <= f[:, :, 1] * (1 + 1e-6))).all())
