@@ -317,6 +317,17 @@ def cpu_decode(wl, x, rows_req):
                       f"({rows} rows); {dt:.1f} s"}
 
 
+def device_peaks():
+    """The device's CU count and clocks, with the peaks derived from them."""
+    from paper_2608_09703_amd import binding as B
+    cu, clk, mclk, bus = B.device_info()
+    return {"compute_units": cu, "clock_mhz": clk / 1e3, "mem_clock_mhz": mclk / 1e3,
+            "mem_bus_bits": bus,
+            "bf16_peak_tflops_nominal": PEAK_FLOPS["bf16"] / 1e12,
+            "bf16_peak_tflops_derived": cu * clk * 1e3 * 4096 / 1e12,
+            "hbm_peak_gbs_nominal": HBM_PEAK / 1e9}
+
+
 def main_decode(args):
     import torch
     from paper_2608_09703_amd import binding as B
@@ -554,6 +565,10 @@ def main():
     pct = flops_step / (ms_step / 1e3) / peak * 100.0
     log(f"{args.steps} steps: {ms_step:.3f} ms/step, {tokens_per_s:,.0f} tokens/s, "
         f"{pct:.1f}% of {wl.dtype} MFMA peak (algorithmic)")
+    device = device_peaks()
+    log(f"peaks: nominal bf16 {PEAK_FLOPS['bf16'] / 1e12:.0f} TFLOP/s, from the device's "
+        f"{device['compute_units']} CUs x {device['clock_mhz']:.0f} MHz x 4096 FLOP/clk: "
+        f"{device['bf16_peak_tflops_derived']:.0f} TFLOP/s")
 
     # per-kernel times from the library's event timer over the timed region
     kernels = {}
@@ -615,6 +630,9 @@ def main():
                    "ignore_frac": wl.ignore_frac, "parallelism": "single GPU"},
         "pct_of_bf16_peak": pct if wl.dtype == "bf16" else None,
         "algorithmic_tflop_per_step": flops_step / 1e12,
+        # forward + backward execute the logits product once more (recompute): 8 T V sum(d)
+        "executed_tflop_per_step": flops_step * (1.0 if args.diagnostics else 4.0 / 3.0) / 1e12,
+        "device": device,
         "roofline": roofline,
         "kernels": kernels,
         "cpu_baseline": cpu,

@@ -357,6 +357,16 @@ const char* mls_last_error(void);
 /* Library version string. */
 const char* mls_version(void);
 
+/*
+ * Host helper: properties of the current device that set its nominal peaks
+ * (compute units, peak engine clock in kHz, peak memory clock in kHz, memory
+ * bus width in bits; from hipDeviceGetAttribute). Any output may be NULL.
+ * The bf16 dense MFMA peak of a gfx950 part is CUs x clock x 4096 FLOP per
+ * clock per CU.
+ */
+mls_status mls_device_info(int32_t* compute_units, int32_t* clock_khz, int32_t* mem_clock_khz,
+                           int32_t* mem_bus_bits);
+
 #ifdef __cplusplus
 }
 #endif

@@ -54,6 +54,7 @@ EXPORTED = (
     "mls_status_string",
     "mls_last_error",
     "mls_version",
+    "mls_device_info",
     "mls_profile_enable",
     "mls_profile_report",
 )
@@ -151,6 +152,8 @@ def lib():
         L.mls_last_error.restype = ctypes.c_char_p
         L.mls_version.argtypes = []
         L.mls_version.restype = ctypes.c_char_p
+        ip = ctypes.POINTER(ctypes.c_int32)
+        L.mls_device_info.argtypes = [ip, ip, ip, ip]
         L.mls_profile_enable.argtypes = [ctypes.c_int32]
         L.mls_profile_report.argtypes = [ctypes.POINTER(KernelTime), ctypes.c_int32,
                                          ctypes.POINTER(ctypes.c_int32)]
@@ -279,6 +282,13 @@ def coeffs(M: int, teacher: int = -1, alpha: float = 0.0, tau: float = 1.0,
     wa = FA(*w) if w is not None else None
     check(lib().mls_coeffs(M, teacher, alpha, tau, mode, wa, g_ce, g_kl), "mls_coeffs")
     return list(g_ce)[:M], list(g_kl)[:M]
+
+
+def device_info():
+    """``(compute_units, clock_khz, mem_clock_khz, mem_bus_bits)`` of the current device."""
+    v = [ctypes.c_int32(0) for _ in range(4)]
+    check(lib().mls_device_info(*[ctypes.byref(x) for x in v]), "mls_device_info")
+    return tuple(x.value for x in v)
 
 
 def read_stats_header(p: Problem, stats: int, stream: int):

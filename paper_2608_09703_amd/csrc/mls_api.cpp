@@ -281,6 +281,29 @@ extern "C" {
 
 const char* mls_version(void) { return "mls 0.1.0 (gfx950)"; }
 
+mls_status mls_device_info(int32_t* compute_units, int32_t* clock_khz, int32_t* mem_clock_khz,
+                           int32_t* mem_bus_bits) {
+  g_last_error.clear();
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  struct Q {
+    int32_t* out;
+    hipDeviceAttribute_t attr;
+  } qs[] = {{compute_units, hipDeviceAttributeMultiprocessorCount},
+            {clock_khz, hipDeviceAttributeClockRate},
+            {mem_clock_khz, hipDeviceAttributeMemoryClockRate},
+            {mem_bus_bits, hipDeviceAttributeMemoryBusWidth}};
+  for (const Q& q : qs) {
+    if (!q.out) continue;
+    int v = 0;
+    if ((e = hipDeviceGetAttribute(&v, q.attr, dev)) != hipSuccess)
+      return hip_fail(e, "hipDeviceGetAttribute");
+    *q.out = v;
+  }
+  return MLS_OK;
+}
+
 const char* mls_last_error(void) { return g_last_error.c_str(); }
 
 const char* mls_status_string(mls_status s) {
