@@ -117,13 +117,15 @@ __global__ __launch_bounds__(Mma::NT, 2) void head_logits_kernel(HeadArgs a) {
 // * for c' > c, S(c') >= S(c) - n(c) c', where n(c) counts the weights at or
 //   above c; so S(c) >= P also gives theta >= (S(c) - P) / n(c).
 // The search starts at c0 = (1 - top_p) total / V (the weights below c0 hold
-// less than (1 - top_p) of the mass, so S(c0) >= P) and raises the bound with
-// the second fact while the candidate set {weight >= c} is large. The
-// candidates are then compacted into LDS in index order, and one wave bisects
-// the fp32 bit pattern over them (positive floats order like their bits),
-// resolves ties and draws: every kept token is a candidate. Rows whose
-// candidate set stays large (flat distributions) take a block-wide search
-// over the whole row.
+// less than (1 - top_p) of the mass, so S(c0) >= P). The candidates
+// {weight >= c0} are compacted once into a first LDS list (each wave its own
+// region, in index order), the bound is raised with the second fact on that
+// list, and the survivors move in index order to the final list. One wave
+// then finds theta over the fp32 bit pattern (positive floats order like
+// their bits) with four-way steps, resolves ties and draws: every kept token
+// is in the final list. Rows whose first list overflows raise the bound over
+// the row's registers instead; rows whose candidate set stays large (flat
+// distributions) take a block-wide search over the whole row.
 
 constexpr int kRowThreads = 1024;
 constexpr int kRowWaves = kRowThreads / 64;
@@ -142,11 +144,11 @@ __device__ __forceinline__ int cand_slot(int j) { return j + (j >> 4); }
 constexpr int kCandSlots = kMaxCand + kMaxCand / 16;
 
 struct RowShared {
-  float bw[kBigCand];             // first list (weights >= c0), index order
-  int bi[kBigCand];
+  float bw[kBigCand];             // first list (weights >= c0): one region per wave,
+  int bi[kBigCand];               // each in index order
   float cw[kCandSlots];           // final list, index order
   int ci[kCandSlots];             // their vocabulary indices
-  float seg[kMaxEPT * kRowWaves]; // per (slab, wave) sums for whole-row index-order scans
+  float seg[kMaxEPT * kRowWaves]; // per (wave, slab) sums for whole-row index-order scans
   float red[kRowWaves];
   int ired[kRowWaves];
   int wcnt[kRowWaves];            // per-wave list counts
@@ -504,7 +506,6 @@ __device__ __forceinline__ int run_draw(const float (&kw)[RUN], float target) {
 // entry remains in [lo, hi), it is theta.
 template <int RUN>
 __device__ __forceinline__ float list_theta(const float (&w)[RUN], float c, float P) {
-  const int lane = threadIdx.x & 63;
   // invariant: S(lo) >= P > S(hi); lo, hi and the decisions are wave-uniform
   uint32_t lo = __float_as_uint(c), hi = 0x3f800001u;  // nothing is above 1
   while (hi - lo > 1) {
@@ -559,7 +560,6 @@ __device__ __forceinline__ float list_theta(const float (&w)[RUN], float c, floa
         hi = mid;
     }
   }
-  (void)lane;
   return __uint_as_float(lo);
 }
 
