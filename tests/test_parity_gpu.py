@@ -171,7 +171,7 @@ def test_autograd_front_end():
 # benchmark workloads at full size
 # ---------------------------------------------------------------------------
 
-FULL = ["c2_m3_v50k", "c3_m3_v128k_tau2", "c4_m4_v128k_peaky", "c5_m3_v262k_long"]
+FULL = ["c2_m3_v50k", "c3_m3_v128k_tau2", "c4_m4_v128k_peaky", "c5_m3_v262k_long", "paper3b_heads"]
 
 
 @pytest.mark.parametrize("name", FULL)
