@@ -246,3 +246,41 @@ def test_full_size_backward_is_bitwise_repeatable(name):
         for i in range(wl.M):
             assert np.array_equal(gpu["grad_W"][i], first["grad_W"][i]), (rep, i)
             assert np.array_equal(gpu["grad_h"][i], first["grad_h"][i]), (rep, i)
+
+
+@pytest.mark.parametrize("dtype,chunk", [("bf16", 512), ("f32", 256)])
+def test_accumulate_flags_and_skipped_gradients(dtype, chunk):
+    """MLS_ACCUMULATE_GRAD_W / _H add to the caller's gradients instead of
+    overwriting them (over several vocabulary chunks), on the wide bf16 and
+    the general fp32 paths; NULL gradient pointers skip those outputs and the
+    others are still right."""
+    from paper_2608_09703_amd import api as D
+    from paper_2608_09703_amd import binding as B
+    wl = WL.custom(3, 200, (64, 128, 192) if dtype == "bf16" else (32, 36, 100), 1100, dtype=dtype,
+                   tau=1.3, w_std=0.08, ignore_frac=0.1, seed=31)
+    print(f"[parity] accumulate flags {dtype} chunk {chunk}", flush=True)
+    h, W, y = WL.make_inputs(wl, device=DEV)
+    ref = run_gpu(h, W, y, tau=wl.tau, vocab_chunk=chunk, alpha=0.4)  # overwrite mode
+    flags = B.MLS_ACCUMULATE_GRAD_W | B.MLS_ACCUMULATE_GRAD_H
+    p = D.make_problem(h, W, y, tau=wl.tau, vocab_chunk=chunk, alpha=0.4, flags=flags)
+    buf = D.Buffers(p, DEV)
+    D.forward(p, buf, DEV)
+    g = torch.Generator(device=DEV).manual_seed(5)
+    # starting values of the gradients' own scale, so that the added part is checked tightly
+    gh0 = [torch.randn(x.shape, generator=g, device=DEV) * float(np.std(r))
+           for x, r in zip(h, ref["grad_h"])]
+    gW0 = [torch.randn(x.shape, generator=g, device=DEV) * float(np.std(r))
+           for x, r in zip(W, ref["grad_W"])]
+    gh = [x.clone() for x in gh0]
+    gW = [x.clone() for x in gW0]
+    gh[1] = None   # no grad_h for sub-model 1
+    gW[2] = None   # no grad_W for sub-model 2
+    D.backward(p, buf, DEV, None, None, gh, gW)
+    torch.cuda.synchronize()
+    for i in range(3):
+        if gh[i] is not None:
+            added = gh[i].cpu().numpy().astype(np.float64) - gh0[i].cpu().numpy()
+            assert rel_fro(added, ref["grad_h"][i]) < 1e-5, f"grad_h {i}"
+        if gW[i] is not None:
+            added = gW[i].cpu().numpy().astype(np.float64) - gW0[i].cpu().numpy()
+            assert rel_fro(added, ref["grad_W"][i]) < 1e-5, f"grad_W {i}"
