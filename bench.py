@@ -9,8 +9,8 @@ eq. (3). Prints one JSON line (see README of the build for the fields).
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 
 With --diagnostics a step is instead the monitoring pass of paper section 3:
-mls_distill_fwd (log-sum-exp rows and losses) + mls_diagnostics (pairwise KL at
-temperature 1 and top-1 agreement of every pair of sub-models).
+mls_diagnostics, one self-normalising pass over every sub-model's logits (pairwise
+KL at temperature 1 and top-1 agreement of every pair of sub-models).
 
 With --junction a step is the forward and backward of every inter-model junction
 (eq. (1)) of a suite (mls_junction_fwd + mls_junction_bwd per junction).
@@ -35,7 +35,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "fused LM-head+CE+KL fwd+bwd tokens/s (M=3, V=50304); % of bf16 MFMA peak"
-METRIC_DIAG = "cross-model diagnostics (fused forward + pairwise KL/top-1 agreement) tokens/s"
+METRIC_DIAG = "cross-model diagnostics (pairwise KL/top-1 agreement, one pass) tokens/s"
 METRIC_JUNCTION = "inter-model junctions fwd+bwd tokens/s (every junction of the suite)"
 METRIC_DECODE = ("speculative head step rows/s (gamma draft steps x batch + verifier "
                  "(gamma + 1) x batch rows)")
@@ -86,7 +86,7 @@ def parse():
     ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample rows (0 = auto)")
     ap.add_argument("--vocab-chunk", type=int, default=0)
     ap.add_argument("--diagnostics", action="store_true",
-                    help="time the forward + pairwise diagnostics pass instead of fwd+bwd")
+                    help="time the pairwise diagnostics pass instead of fwd+bwd")
     ap.add_argument("--junction", action="store_true",
                     help="time the inter-model junctions (forward + backward) instead")
     ap.add_argument("--decode", action="store_true",
@@ -98,8 +98,8 @@ def parse():
 
 
 def cpu_baseline(wl, h, W, y, g_ce, g_kl, rows_req, diagnostics=False):
-    """Times the float64 CPU oracle (forward + backward, or forward + diagnostics)
-    on a sample of rows."""
+    """Times the float64 CPU oracle (forward + backward, or the diagnostics) on a
+    sample of rows."""
     import numpy as np
     import oracle
 
@@ -116,10 +116,10 @@ def cpu_baseline(wl, h, W, y, g_ce, g_kl, rows_req, diagnostics=False):
         hn = [x[:nrows].float().cpu().numpy() for x in h]
         yn = yn_all[:nrows]
         t0 = time.perf_counter()
-        oracle.forward(hn, Wn, yn, tau=wl.tau)
         if diagnostics:
             oracle.diagnostics(hn, Wn, yn)
         else:
+            oracle.forward(hn, Wn, yn, tau=wl.tau)
             oracle.backward(hn, Wn, yn, g_ce, g_kl, tau=wl.tau)
         return time.perf_counter() - t0
 
@@ -141,7 +141,7 @@ def cpu_baseline(wl, h, W, y, g_ce, g_kl, rows_req, diagnostics=False):
         "unit": "tokens/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": f"float64 numpy oracle, forward + {'diagnostics' if diagnostics else 'backward'} "
+        "sample": f"float64 numpy oracle, {'diagnostics' if diagnostics else 'forward + backward'} "
                   f"on the first {rows} of {wl.T} tokens "
                   f"at full V={wl.V} and widths {list(wl.dims)}; {dt:.1f} s",
     }
@@ -532,12 +532,12 @@ def main():
     agree = torch.empty(wl.M, wl.M, dtype=torch.float32, device=dev)
 
     def step():
+        if args.diagnostics:
+            B.diagnostics(p, kl_pair.data_ptr(), agree.data_ptr(), None, ws_ptr, ws_n, sh)
+            return
         B.distill_fwd(p, st_ptr, buf.ce.data_ptr(), buf.kl.data_ptr(), buf.entropy.data_ptr(),
                       ws_ptr, ws_n, sh)
-        if args.diagnostics:
-            B.diagnostics(p, st_ptr, kl_pair.data_ptr(), agree.data_ptr(), None, ws_ptr, ws_n, sh)
-        else:
-            B.distill_bwd(p, st_ptr, gce.data_ptr(), gkl.data_ptr(), gh_p, gW_p, ws_ptr, ws_n, sh)
+        B.distill_bwd(p, st_ptr, gce.data_ptr(), gkl.data_ptr(), gh_p, gW_p, ws_ptr, ws_n, sh)
 
     log(f"workspace {ws_n / 2**20:.0f} MiB, stats {buf.stats.numel() / 2**20:.1f} MiB")
     for k in range(args.warmup):
@@ -559,8 +559,8 @@ def main():
     ms_total = t0.elapsed_time(t1)
     ms_step = ms_total / args.steps
     tokens_per_s = wl.T / (ms_step / 1e3)
-    # forward + backward: 6*T*V*sum(d); forward + diagnostics: two 2*T*V*sum(d) passes
-    flops_step = wl.algorithmic_flops() * (2.0 / 3.0 if args.diagnostics else 1.0)
+    # forward + backward: 6*T*V*sum(d); diagnostics: one 2*T*V*sum(d) pass
+    flops_step = wl.algorithmic_flops() * (1.0 / 3.0 if args.diagnostics else 1.0)
     peak = PEAK_FLOPS[wl.dtype]
     pct = flops_step / (ms_step / 1e3) / peak * 100.0
     log(f"{args.steps} steps: {ms_step:.3f} ms/step, {tokens_per_s:,.0f} tokens/s, "

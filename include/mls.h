@@ -177,15 +177,14 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
  *   kl_pair[i*M + j] = mean KL(softmax(l_i) || softmax(l_j))   (temperature 1)
  *   agree[i*M + j]   = mean [argmax_v l_i == argmax_v l_j]     (ties: lowest index)
  * kl_pair and agree are device float32 [M*M]; argmax (device int32 [M][T], may be
- * NULL) receives every token's top-1 index per sub-model. `stats` must come from
- * mls_distill_fwd on the same inputs (its log-sum-exp rows are reused; tau and
+ * NULL) receives every token's top-1 index per sub-model. One pass over the
+ * logits, normalised as it goes: no forward statistics are needed (tau and
  * teacher do not matter here). The workspace of mls_query_sizes suffices.
  * M must be at most 4 (MLS_UNSUPPORTED otherwise). With no valid token the
  * outputs are 0. Asynchronous on stream.
  */
-mls_status mls_diagnostics(const mls_problem* p, const void* stats, float* kl_pair, float* agree,
-                           int32_t* argmax, void* workspace, size_t workspace_bytes,
-                           void* stream);
+mls_status mls_diagnostics(const mls_problem* p, float* kl_pair, float* agree, int32_t* argmax,
+                           void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * Inter-model junction (paper section 2, "Inter-model Junction", eq. (1)):

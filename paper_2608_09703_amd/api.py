@@ -155,8 +155,8 @@ def distill(h_list: Sequence[torch.Tensor], W_list: Sequence[torch.Tensor], labe
 
 def run_diagnostics(p: B.Problem, buf: Buffers, device, kl_pair: torch.Tensor, agree: torch.Tensor,
                     argmax: Optional[torch.Tensor]) -> None:
-    """Pairwise diagnostics into caller tensors; ``buf.stats`` must hold this problem's forward."""
-    B.diagnostics(p, buf.stats.data_ptr(), kl_pair.data_ptr(), agree.data_ptr(),
+    """Pairwise diagnostics into caller tensors (one pass; ``buf.workspace`` is used)."""
+    B.diagnostics(p, kl_pair.data_ptr(), agree.data_ptr(),
                   argmax.data_ptr() if argmax is not None else None, buf.workspace.data_ptr(),
                   buf.workspace.numel(), _stream(device))
 
@@ -168,12 +168,11 @@ def diagnostics(h_list: Sequence[torch.Tensor], W_list: Sequence[torch.Tensor],
 
     ``kl[i, j]`` is the mean over valid tokens of KL(p_i || p_j) at temperature 1 and
     ``agree[i, j]`` the fraction of valid tokens whose top-1 predictions coincide.
-    Runs the fused forward (for the log-sum-exp rows) and then the pairwise pass.
+    One self-normalising pass over the logits of all sub-models.
     """
     p = make_problem(h_list, W_list, labels, ignore_index=ignore_index)
     dev = h_list[0].device
     buf = Buffers(p, dev)
-    forward(p, buf, dev)
     M, T = len(h_list), h_list[0].shape[0]
     kl = torch.empty(M, M, dtype=torch.float32, device=dev)
     agree = torch.empty(M, M, dtype=torch.float32, device=dev)

@@ -130,7 +130,7 @@ def lib():
         L.mls_distill_fwd.argtypes = [P, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
         L.mls_distill_bwd.argtypes = [P, vp, vp, vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp,
                                       ctypes.c_size_t, vp]
-        L.mls_diagnostics.argtypes = [P, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        L.mls_diagnostics.argtypes = [P, vp, vp, vp, vp, ctypes.c_size_t, vp]
         J = ctypes.POINTER(Junction)
         L.mls_junction_fwd.argtypes = [J, vp, vp, vp, vp]
         L.mls_junction_bwd.argtypes = [J, vp, vp, vp, vp, vp, vp]
@@ -217,10 +217,10 @@ def distill_bwd(p: Problem, stats: int, g_ce: Optional[int], g_kl: Optional[int]
                                 stream), "mls_distill_bwd")
 
 
-def diagnostics(p: Problem, stats: int, kl_pair: int, agree: int, argmax: Optional[int], ws: int,
+def diagnostics(p: Problem, kl_pair: int, agree: int, argmax: Optional[int], ws: int,
                 ws_bytes: int, stream: int):
-    check(lib().mls_diagnostics(ctypes.byref(p), stats, kl_pair, agree, argmax, ws, ws_bytes,
-                                stream), "mls_diagnostics")
+    check(lib().mls_diagnostics(ctypes.byref(p), kl_pair, agree, argmax, ws, ws_bytes, stream),
+          "mls_diagnostics")
 
 
 def make_junction(T: int, d_prev: int, d_fresh: int, act_dtype: int = MLS_BF16,

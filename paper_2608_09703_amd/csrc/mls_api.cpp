@@ -593,19 +593,17 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
   return MLS_OK;
 }
 
-mls_status mls_diagnostics(const mls_problem* p, const void* stats, float* kl_pair, float* agree,
-                           int32_t* argmax, void* workspace, size_t workspace_bytes,
-                           void* stream) {
+mls_status mls_diagnostics(const mls_problem* p, float* kl_pair, float* agree, int32_t* argmax,
+                           void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error.clear();
   mls_status st = validate(p);
   if (st != MLS_OK) return st;
   if (p->M > kMaxDiagModels)
     return fail(MLS_UNSUPPORTED, "diagnostics support M <= %d, got %d", kMaxDiagModels, p->M);
-  if (!stats || !kl_pair || !agree || !workspace)
-    return fail(MLS_INVALID_ARG, "stats, kl_pair, agree and workspace must be non-NULL");
-  if (!aligned(stats, 16) || !aligned(workspace, 16) || !aligned(kl_pair, 4) || !aligned(agree, 4) ||
-      !aligned(argmax, 4))
-    return fail(MLS_INVALID_ARG, "misaligned stats / workspace / output pointer");
+  if (!kl_pair || !agree || !workspace)
+    return fail(MLS_INVALID_ARG, "kl_pair, agree and workspace must be non-NULL");
+  if (!aligned(workspace, 16) || !aligned(kl_pair, 4) || !aligned(agree, 4) || !aligned(argmax, 4))
+    return fail(MLS_INVALID_ARG, "misaligned workspace / output pointer");
   Plan pl;
   make_plan(p, pl);
   if (workspace_bytes < pl.diag_bytes)
@@ -624,7 +622,6 @@ mls_status mls_diagnostics(const mls_problem* p, const void* stats, float* kl_pa
   a.V = p->V;
   a.labels = p->labels;
   a.ignore_index = p->ignore_index;
-  a.lse1 = static_cast<const float*>(stats);  // lse1[M][T] leads the statistics
   a.n_tt = pl.n_tt_diag;
   a.n_vt = pl.n_vt_diag;
   a.group_v = 8;

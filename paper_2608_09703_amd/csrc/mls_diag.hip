@@ -3,15 +3,18 @@
 // tokens of KL(p_i || p_j) at temperature 1 and the rate at which their top-1
 // next-token predictions agree (argmax ties go to the lowest vocabulary index).
 //
-// One block owns one (vocabulary tile, token tile) pair, as the fused forward
-// does, and computes the logits tile of every sub-model (all M accumulator sets
-// stay in registers, M <= 4). Then, per logit:
-//   p_i = exp(l_i - lse_i)          (lse_i from the forward statistics)
-//   D_ij += p_i (l_i - l_j)         for every ordered pair i != j
-//   running argmax of l_i
-// and writes one record per token of the tile. Per token, after the records of
-// all vocabulary tiles are summed, KL(p_i || p_j) = D_ij - lse_i + lse_j. No
-// [T, V] tensor is formed.
+// One pass, normalising itself. One block owns one (vocabulary tile, token
+// tile) pair, as the fused forward does, and computes the logits tile of every
+// sub-model (all M accumulator sets stay in registers, M <= 4). Per token and
+// sub-model i, relative to the largest logit m_i seen so far:
+//   Z_i  = sum_v exp(l_i - m_i)
+//   S_ij = sum_v exp(l_i - m_i) (l_i - l_j)      for every ordered pair i != j
+// and the argmax of l_i (its value is m_i). Two partial results (m, Z, S) and
+// (m', Z', S') merge as m'' = max(m, m'), Z'' = Z e^{m - m''} + Z' e^{m' - m''},
+// S'' likewise with the scale of model i. Across lanes, waves, vocabulary tiles
+// and slices the same merge applies; at the end, with lse_i = m_i + log Z_i,
+//   KL(p_i || p_j) = sum_v p_i (l_i - l_j) - lse_i + lse_j = S_ij / Z_i - lse_i + lse_j.
+// No [T, V] tensor is formed and no forward statistics are needed.
 #include <math.h>
 
 #include "mls_core.h"
@@ -24,8 +27,35 @@ namespace {
 
 template <int MM>
 struct DiagRec {
-  static constexpr int kFloats = MM * MM + 2 * MM;  // D[MM][MM], best[MM], index[MM]
+  // per (vocabulary tile, token): S[MM][MM], Z[MM], best (= m)[MM], index[MM]
+  static constexpr int kS = 0;
+  static constexpr int kZ = MM * MM;
+  static constexpr int kBest = MM * MM + MM;
+  static constexpr int kIdx = MM * MM + 2 * MM;
+  static constexpr int kFloats = MM * MM + 3 * MM;
 };
+
+// e^{x - m} for x <= m, where x = -inf marks an empty partial (its sums are 0)
+__device__ __forceinline__ float rescale(float x, float m) {
+  return x == -INFINITY ? 0.f : fast_exp2((x - m) * kLog2e);
+}
+
+// Merges partial (ob, oi, oz, os) into (b, bi, z, s) for one sub-model i; os/s
+// are its MM pair sums S_i*.
+template <int MM>
+__device__ __forceinline__ void merge_part(float& b, int& bi, float& z, float* s, float ob, int oi,
+                                           float oz, const float* os) {
+  const float m = fmaxf(b, ob);
+  const float sa = rescale(b, m);
+  const float sb = rescale(ob, m);
+  z = z * sa + oz * sb;
+#pragma unroll
+  for (int j = 0; j < MM; ++j) s[j] = s[j] * sa + os[j] * sb;
+  if (ob > b || (ob == b && oi < bi)) {
+    b = ob;
+    bi = oi;
+  }
+}
 
 template <class Mma, typename E, int MM, int MINB>
 __global__ __launch_bounds__(Mma::NT, MINB) void diag_tile_kernel(DiagArgs a) {
@@ -34,9 +64,12 @@ __global__ __launch_bounds__(Mma::NT, MINB) void diag_tile_kernel(DiagArgs a) {
   constexpr int WGM = Mma::kWGM;
   constexpr int FM = Mma::FM;
   constexpr int FN = Mma::FN;
-  constexpr int REC = DiagRec<MM>::kFloats;
+  using R = DiagRec<MM>;
+  constexpr int REC = R::kFloats;
   __shared__ __attribute__((aligned(16))) char smem[Mma::kSmemBytes];
-  __shared__ float red[WGM][BN][REC];
+  // the per-wave partials of the epilogue reuse the operand staging buffer
+  static_assert(sizeof(float) * WGM * BN * REC <= Mma::kSmemBytes, "epilogue partials overflow LDS");
+  auto red = reinterpret_cast<float (*)[BN][REC]>(smem);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -58,22 +91,42 @@ __global__ __launch_bounds__(Mma::NT, MINB) void diag_tile_kernel(DiagArgs a) {
     mma[j].run(static_cast<const char*>(a.W[j]), kb, vbase, a.V, static_cast<const char*>(a.h[j]),
                kb, tbase, a.T, kb, smem, tid);
   }
+  __syncthreads();  // every wave is done reading operands from smem
 
 #pragma unroll
   for (int fn = 0; fn < FN; ++fn) {
-    const int64_t t = tbase + Mma::col_of(wn, fn, lane);
-    float lse[MM];
-#pragma unroll
-    for (int i = 0; i < MM; ++i) lse[i] = t < a.T ? a.lse1[(int64_t)i * a.T + t] * kLog2e : 0.f;
-    float D[MM][MM];
+    // first sweep over the lane's rows: argmax, whose value is the lane's maximum
     float best[MM];
     int bidx[MM];
 #pragma unroll
     for (int i = 0; i < MM; ++i) {
       best[i] = -INFINITY;
       bidx[i] = 0x7fffffff;
+    }
 #pragma unroll
-      for (int j = 0; j < MM; ++j) D[i][j] = 0.f;
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int v = (int)vbase + Mma::row_of(wm, fm, r, lane);
+        const bool ok = full || v < a.V;
+#pragma unroll
+        for (int i = 0; i < MM; ++i) {
+          const float l = mma[i].acc[fm][fn][r];
+          // rows are visited in increasing order within a lane: strict > keeps the lowest
+          if (ok && l > best[i]) {
+            best[i] = l;
+            bidx[i] = v;
+          }
+        }
+      }
+    // second sweep: sums relative to that maximum (a lane with no row keeps 0)
+    float mb[MM], Z[MM], S[MM][MM];
+#pragma unroll
+    for (int i = 0; i < MM; ++i) {
+      mb[i] = best[i] == -INFINITY ? 0.f : best[i] * kLog2e;
+      Z[i] = 0.f;
+#pragma unroll
+      for (int j = 0; j < MM; ++j) S[i][j] = 0.f;
     }
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
@@ -85,150 +138,143 @@ __global__ __launch_bounds__(Mma::NT, MINB) void diag_tile_kernel(DiagArgs a) {
 #pragma unroll
         for (int i = 0; i < MM; ++i) {
           l[i] = mma[i].acc[fm][fn][r];
-          p[i] = ok ? fast_exp2(fmaf(l[i], kLog2e, -lse[i])) : 0.f;
+          p[i] = ok ? fast_exp2(fmaf(l[i], kLog2e, -mb[i])) : 0.f;
+          Z[i] += p[i];
         }
 #pragma unroll
-        for (int i = 0; i < MM; ++i) {
+        for (int i = 0; i < MM; ++i)
 #pragma unroll
           for (int j = 0; j < MM; ++j)
-            if (j != i) D[i][j] = fmaf(p[i], l[i] - l[j], D[i][j]);
-          // rows are visited in increasing order within a lane: strict > keeps the lowest
-          if (ok && l[i] > best[i]) {
-            best[i] = l[i];
-            bidx[i] = v;
-          }
-        }
+            if (j != i) S[i][j] = fmaf(p[i], l[i] - l[j], S[i][j]);
       }
 
-    // lanes l and l ^ 32 hold the same token column: combine, then the WGM
-    // waves of the column through LDS
+    // lanes l and l ^ 32 hold the same token column: merge, then the WGM waves
+    // of the column through LDS
 #pragma unroll
     for (int i = 0; i < MM; ++i) {
+      float os[MM];
 #pragma unroll
-      for (int j = 0; j < MM; ++j) D[i][j] += __shfl_xor(D[i][j], 32, 64);
+      for (int j = 0; j < MM; ++j) os[j] = __shfl_xor(S[i][j], 32, 64);
+      const float oz = __shfl_xor(Z[i], 32, 64);
       const float ob = __shfl_xor(best[i], 32, 64);
       const int oi = __shfl_xor(bidx[i], 32, 64);
-      if (ob > best[i] || (ob == best[i] && oi < bidx[i])) {
-        best[i] = ob;
-        bidx[i] = oi;
-      }
+      merge_part<MM>(best[i], bidx[i], Z[i], S[i], ob, oi, oz, os);
     }
     if (hi == 0) {
       const int c = Mma::col_of(wn, fn, lane);
 #pragma unroll
       for (int i = 0; i < MM; ++i) {
 #pragma unroll
-        for (int j = 0; j < MM; ++j) red[wm][c][i * MM + j] = D[i][j];
-        red[wm][c][MM * MM + i] = best[i];
-        red[wm][c][MM * MM + MM + i] = __int_as_float(bidx[i]);
+        for (int j = 0; j < MM; ++j) red[wm][c][R::kS + i * MM + j] = S[i][j];
+        red[wm][c][R::kZ + i] = Z[i];
+        red[wm][c][R::kBest + i] = best[i];
+        red[wm][c][R::kIdx + i] = __int_as_float(bidx[i]);
       }
     }
   }
   __syncthreads();
-  // record layout [vocabulary tile][field][token]: consecutive threads write
-  // consecutive tokens
-  for (int idx = tid; idx < BN * (MM * MM + MM); idx += Mma::NT) {
+  // merge the WGM waves of a column and write the record, layout
+  // [vocabulary tile][field][token]: consecutive threads write consecutive
+  // tokens. One thread takes one (token, sub-model) pair.
+  for (int idx = tid; idx < BN * MM; idx += Mma::NT) {
     const int c = idx % BN;
-    const int q = idx / BN;  // 0..MM*MM-1: D sums, MM*MM..: argmax
+    const int i = idx / BN;
     const int64_t t = tbase + c;
     if (t >= a.T) continue;
-    float* out = a.partials + (int64_t)vt * REC * a.T;
-    if (q < MM * MM) {
-      float sum = 0.f;
+    float b = red[0][c][R::kBest + i];
+    int bi = __float_as_int(red[0][c][R::kIdx + i]);
+    float z = red[0][c][R::kZ + i];
+    float s[MM];
 #pragma unroll
-      for (int w = 0; w < WGM; ++w) sum += red[w][c][q];
-      out[(int64_t)q * a.T + t] = sum;
-    } else {
-      const int i = q - MM * MM;
-      float b = red[0][c][MM * MM + i];
-      int bi = __float_as_int(red[0][c][MM * MM + MM + i]);
+    for (int j = 0; j < MM; ++j) s[j] = red[0][c][R::kS + i * MM + j];
 #pragma unroll
-      for (int w = 1; w < WGM; ++w) {
-        const float ob = red[w][c][MM * MM + i];
-        const int oi = __float_as_int(red[w][c][MM * MM + MM + i]);
-        if (ob > b || (ob == b && oi < bi)) {
-          b = ob;
-          bi = oi;
-        }
-      }
-      out[(int64_t)(MM * MM + i) * a.T + t] = b;
-      out[(int64_t)(MM * MM + MM + i) * a.T + t] = __int_as_float(bi);
+    for (int w = 1; w < WGM; ++w) {
+      float os[MM];
+#pragma unroll
+      for (int j = 0; j < MM; ++j) os[j] = red[w][c][R::kS + i * MM + j];
+      merge_part<MM>(b, bi, z, s, red[w][c][R::kBest + i], __float_as_int(red[w][c][R::kIdx + i]),
+                     red[w][c][R::kZ + i], os);
     }
+    float* out = a.partials + (int64_t)vt * REC * a.T + t;
+#pragma unroll
+    for (int j = 0; j < MM; ++j) out[(int64_t)(R::kS + i * MM + j) * a.T] = s[j];
+    out[(int64_t)(R::kZ + i) * a.T] = z;
+    out[(int64_t)(R::kBest + i) * a.T] = b;
+    out[(int64_t)(R::kIdx + i) * a.T] = __int_as_float(bi);
   }
 }
 
-// Per token: sum the records of all vocabulary tiles, finish KL(p_i || p_j) and
-// the argmax, and write the per-token values the mean reduction reads. A block
-// takes kRowTok tokens; its kRowSlices thread rows each sum every kRowSlices-th
-// vocabulary tile, and the slices are combined in a fixed order.
+// Per token: merge the records of all vocabulary tiles, finish KL(p_i || p_j)
+// and the argmax, and write the per-token values the mean reduction reads. A
+// block takes kRowTok tokens; its kRowSlices thread rows each merge every
+// kRowSlices-th vocabulary tile, and the slices are merged in a fixed order.
 constexpr int kRowTok = 32;
 constexpr int kRowSlices = 8;
 
 template <int MM>
 __global__ __launch_bounds__(kRowTok * kRowSlices) void diag_rows_kernel(DiagArgs a) {
-  constexpr int REC = DiagRec<MM>::kFloats;
+  using R = DiagRec<MM>;
+  constexpr int REC = R::kFloats;
   __shared__ float sh[kRowSlices][REC][kRowTok];
   const int c = threadIdx.x % kRowTok;
   const int g = threadIdx.x / kRowTok;
   const int64_t t = (int64_t)blockIdx.x * kRowTok + c;
-  float D[MM * MM];
-  float best[MM];
+  float S[MM][MM], Z[MM], best[MM];
   int bidx[MM];
-#pragma unroll
-  for (int q = 0; q < MM * MM; ++q) D[q] = 0.f;
 #pragma unroll
   for (int i = 0; i < MM; ++i) {
     best[i] = -INFINITY;
     bidx[i] = 0x7fffffff;
+    Z[i] = 0.f;
+#pragma unroll
+    for (int j = 0; j < MM; ++j) S[i][j] = 0.f;
   }
   if (t < a.T) {
     for (int vt = g; vt < a.n_vt; vt += kRowSlices) {
       const float* in = a.partials + (int64_t)vt * REC * a.T + t;
 #pragma unroll
-      for (int q = 0; q < MM * MM; ++q) D[q] += in[(int64_t)q * a.T];
-#pragma unroll
       for (int i = 0; i < MM; ++i) {
-        const float ob = in[(int64_t)(MM * MM + i) * a.T];
-        const int oi = __float_as_int(in[(int64_t)(MM * MM + MM + i) * a.T]);
-        if (ob > best[i] || (ob == best[i] && oi < bidx[i])) {
-          best[i] = ob;
-          bidx[i] = oi;
-        }
+        float os[MM];
+#pragma unroll
+        for (int j = 0; j < MM; ++j) os[j] = in[(int64_t)(R::kS + i * MM + j) * a.T];
+        merge_part<MM>(best[i], bidx[i], Z[i], S[i], in[(int64_t)(R::kBest + i) * a.T],
+                       __float_as_int(in[(int64_t)(R::kIdx + i) * a.T]),
+                       in[(int64_t)(R::kZ + i) * a.T], os);
       }
     }
   }
 #pragma unroll
-  for (int q = 0; q < MM * MM; ++q) sh[g][q][c] = D[q];
-#pragma unroll
   for (int i = 0; i < MM; ++i) {
-    sh[g][MM * MM + i][c] = best[i];
-    sh[g][MM * MM + MM + i][c] = __int_as_float(bidx[i]);
+#pragma unroll
+    for (int j = 0; j < MM; ++j) sh[g][R::kS + i * MM + j][c] = S[i][j];
+    sh[g][R::kZ + i][c] = Z[i];
+    sh[g][R::kBest + i][c] = best[i];
+    sh[g][R::kIdx + i][c] = __int_as_float(bidx[i]);
   }
   __syncthreads();
   if (g != 0 || t >= a.T) return;
   for (int w = 1; w < kRowSlices; ++w) {
 #pragma unroll
-    for (int q = 0; q < MM * MM; ++q) D[q] += sh[w][q][c];
-#pragma unroll
     for (int i = 0; i < MM; ++i) {
-      const float ob = sh[w][MM * MM + i][c];
-      const int oi = __float_as_int(sh[w][MM * MM + MM + i][c]);
-      if (ob > best[i] || (ob == best[i] && oi < bidx[i])) {
-        best[i] = ob;
-        bidx[i] = oi;
-      }
+      float os[MM];
+#pragma unroll
+      for (int j = 0; j < MM; ++j) os[j] = sh[w][R::kS + i * MM + j][c];
+      merge_part<MM>(best[i], bidx[i], Z[i], S[i], sh[w][R::kBest + i][c],
+                     __float_as_int(sh[w][R::kIdx + i][c]), sh[w][R::kZ + i][c], os);
     }
   }
   const int64_t y = a.labels[t];
   const bool valid = y != a.ignore_index && y >= 0 && y < a.V;
+  float lse[MM];
+#pragma unroll
+  for (int i = 0; i < MM; ++i) lse[i] = best[i] + logf(Z[i]);
   float* row = a.rowvals + t * (2 * MM * MM);
 #pragma unroll
   for (int i = 0; i < MM; ++i) {
-    const float li = a.lse1[(int64_t)i * a.T + t];
+    const float invz = 1.f / Z[i];
 #pragma unroll
     for (int j = 0; j < MM; ++j) {
-      const float lj = a.lse1[(int64_t)j * a.T + t];
-      row[i * MM + j] = (valid && i != j) ? D[i * MM + j] - li + lj : 0.f;
+      row[i * MM + j] = (valid && i != j) ? S[i][j] * invz - lse[i] + lse[j] : 0.f;
       row[MM * MM + i * MM + j] = (valid && bidx[i] == bidx[j]) ? 1.f : 0.f;
     }
     if (a.argmax) a.argmax[(int64_t)i * a.T + t] = bidx[i];
@@ -319,7 +365,7 @@ hipError_t launch_reduce_m(const DiagArgs& a, hipStream_t stream) {
 
 int diag_tile_rows(bool wide) { return wide ? kFusedWideBM : kFusedBM; }
 int diag_tile_cols(bool wide) { return wide ? kDiagBN : kDiagGenBN; }
-int diag_record_floats(int M) { return M * M + 2 * M; }
+int diag_record_floats(int M) { return M * M + 3 * M; }
 
 hipError_t launch_diag_tiles(const DiagArgs& a, bool f32, bool wide, hipStream_t stream) {
   switch (a.M) {

@@ -146,11 +146,10 @@ struct DiagArgs {
   int64_t V;
   const int64_t* labels;
   int64_t ignore_index;
-  const float* lse1;  // [M][T] from the forward statistics
   int32_t n_tt;
   int32_t n_vt;
   int32_t group_v;        // tile order: vocabulary tiles per group
-  float* partials;        // [n_vt][M*M + 2M][T]
+  float* partials;        // [n_vt][M*M + 3M][T]
   float* rowvals;         // [T][2*M*M]
   float* kl_pair;         // [M][M]
   float* agree;           // [M][M]

@@ -177,18 +177,18 @@ def test_diagnostics_reject_bad_arguments_before_device_work():
     p = _fake_problem(M=5)
     ws, _ = B.query_sizes(p)
     with pytest.raises(B.MlsError) as e:  # more sub-models than the pairwise pass holds
-        B.diagnostics(p, fake, out, out + 256, None, fake + (1 << 20), ws, None)
+        B.diagnostics(p, out, out + 256, None, fake + (1 << 20), ws, None)
     assert e.value.status == B.MLS_UNSUPPORTED
     p = _fake_problem()
     ws, _ = B.query_sizes(p)
     with pytest.raises(B.MlsError) as e:
-        B.diagnostics(p, fake, None, out, None, fake + (1 << 20), ws, None)
+        B.diagnostics(p, None, out, None, fake + (1 << 20), ws, None)
     assert e.value.status == B.MLS_INVALID_ARG
     with pytest.raises(B.MlsError) as e:
-        B.diagnostics(p, fake, out, out + 256, out + 513, fake + (1 << 20), ws, None)
+        B.diagnostics(p, out, out + 256, out + 513, fake + (1 << 20), ws, None)
     assert e.value.status == B.MLS_INVALID_ARG  # misaligned argmax
     with pytest.raises(B.MlsError) as e:
-        B.diagnostics(p, fake, out, out + 256, None, fake + (1 << 20), 16, None)
+        B.diagnostics(p, out, out + 256, None, fake + (1 << 20), 16, None)
     assert e.value.status == B.MLS_WORKSPACE_TOO_SMALL
 
 

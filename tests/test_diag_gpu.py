@@ -104,6 +104,12 @@ SMALL = [
                                 ignore_frac=0.1, seed=27), True),
     ("v2_binary", WL.custom(2, 64, (8, 16), 2, w_std=0.5, seed=28), True),
     ("t1_single_token", WL.custom(3, 1, (64, 64, 128), 300, w_std=0.1, seed=29), False),
+    # logits of standard deviation ~20: every partial is normalised to its own
+    # maximum, and merging rescales across lanes, waves and vocabulary tiles
+    ("m3_large_logits", WL.custom(3, 200, (64, 128, 192), 1500, w_std=None, w_scale=20.0,
+                                  ignore_frac=0.1, seed=30), True),
+    ("m4_large_logits", WL.custom(4, 150, (64, 64, 128, 256), 1100, w_std=None, w_scale=20.0,
+                                  seed=36), False),
 ]
 
 
