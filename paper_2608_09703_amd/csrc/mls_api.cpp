@@ -533,7 +533,10 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
       g.C = grad_h[i];
       g.ldc = p->d[i];
       g.ldc_rows = pl.T;
-      g.K = pl.Vc;
+      // the chunk's rows past vrows read as zero from the head: the last,
+      // shorter chunk stops at the K-tile holding its last row
+      const int64_t kt = gemm_wide_k_tile();
+      g.K = pl.wide ? std::min(pl.Vc, (vrows + kt - 1) / kt * kt) : pl.Vc;
       g.kind = 0;
       g.tiles_m = (int)((pl.T + tbm - 1) / tbm);
       g.tiles_n = (int)((p->d[i] + tbn - 1) / tbn);

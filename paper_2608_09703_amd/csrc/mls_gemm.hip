@@ -155,6 +155,7 @@ __global__ __launch_bounds__(kThreads) void transpose_kernel(TransposeArgs a) {
 
 int gemm_tile_rows(bool wide) { return wide ? kWideBM : kGemmBM; }
 int gemm_tile_cols(bool wide) { return wide ? kWideBN : kGemmBN; }
+int gemm_wide_k_tile() { return WideGemmH::BK; }
 
 hipError_t launch_gemm_wide(const GemmArgs& a, int total_tiles, hipStream_t stream) {
   if (total_tiles <= 0) return hipSuccess;

@@ -242,6 +242,7 @@ hipError_t launch_gemm_wide(const GemmArgs& a, int total_tiles, hipStream_t stre
 hipError_t launch_gemm_nt(const GemmArgs& a, int total_tiles, bool f32, hipStream_t stream);
 hipError_t launch_transpose(const TransposeArgs& a, int64_t max_out_rows, int64_t max_cols,
                             bool f32, hipStream_t stream);
+int gemm_wide_k_tile();  // K values per K-tile of the wide gradient GEMM
 int diag_tile_rows(bool wide);
 int diag_tile_cols(bool wide);
 int diag_record_floats(int M);
