@@ -4,7 +4,8 @@
 One step = mls_distill_fwd + mls_distill_bwd over one batch of synthetic input that is
 already resident in HBM: every sub-model's logits, online log-sum-exp, cross-entropy,
 teacher-to-student KL, and the gradients grad_h_i and grad_W_i with the coefficients of
-eq. (3). Prints one JSON line (see README of the build for the fields).
+eq. (3). Prints one JSON line: throughput, per-kernel times, the roofline of the
+dominant kernel and the CPU oracle's rate on a sample.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 
@@ -495,8 +496,9 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not part "
-                                   "of it (see the sharding design note)", "n_gpus": args.gpus}))
+        print(json.dumps({"error": "the library runs on one GPU; a vocabulary-parallel split over "
+                                   "several GPUs is designed but not implemented",
+                          "n_gpus": args.gpus}))
         sys.exit(2)
     if args.junction:
         return main_junction(args)

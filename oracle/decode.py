@@ -18,7 +18,7 @@ position after the drafts. Greedy verification keeps a draft token while it
 equals the verifier's argmax, and emits the verifier's argmax at the first
 mismatch (or after the last draft).
 
-Readings taken where the paper does not fix the details (listed in the design doc):
+Readings taken where the paper does not fix the details:
 
 * Sampling distribution: ``softmax(l / temperature)``, then the nucleus filter
   keeps the highest-probability tokens, in decreasing probability with ties in

@@ -12,7 +12,7 @@ Euclidean norm equals that of the fresh input embedding ``e`` of sub-model
     o_tilde = o * ||e|| / ||o||                     (per token)
     x       = concat(o_tilde, e)   or   concat(e, o_tilde)
 
-Readings taken where the paper is ambiguous or silent (listed in the design doc):
+Readings taken where the paper is ambiguous or silent:
 
 * Channel order. Eq. (1) writes ``concat(e, o_tilde)``, while the sentence
   after it places sub-model ``m``'s information in the first ``D_m`` channels

@@ -19,7 +19,7 @@ What is computed (paper: "Matryoshka Language Model Suites", section 2,
   weights follow appendix G ("Closing the Per-Size Gap with Loss
   Weighting").
 
-Readings taken where the paper is silent (each is listed in the design doc):
+Readings taken where the paper is silent:
 
 * Temperature ``tau``: the teacher distribution is ``q = softmax(l_s / tau)``
   and the student is ``p_i^tau = softmax(l_i / tau)``; cross-entropy always
