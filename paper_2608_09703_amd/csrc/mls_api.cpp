@@ -502,6 +502,13 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
     }
 
     a.v0 = v0;
+    if (pl.wide) {
+      // The wide GEMM reads slab columns past the chunk's rows only up to the
+      // K-tile holding its last row (grad_h) or for output rows it does not
+      // store (grad_W), so the vocabulary tiles past the chunk end are skipped.
+      const int bm = fused_tile_rows(true);
+      if (bm % gemm_wide_k_tile() == 0) a.n_vt = (int)((vrows + bm - 1) / bm);
+    }
     {
       ProfScope ps("fused_bwd", s);
       e = launch_fused_bwd(a, pl.f32, s);
