@@ -102,7 +102,12 @@ enum mls_device_flags {
  *   vocab_chunk   backward vocabulary chunk width, rounded up to a multiple of
  *                 256; 0 = chosen by the library: at least four balanced
  *                 chunks (more if one chunk's bf16 logit-gradient slabs would
- *                 pass 4 GiB), so no slab spans the whole vocabulary
+ *                 pass 4 GiB), so no slab spans the whole vocabulary. On the
+ *                 bf16 path (every d_i a multiple of 64) the width is also
+ *                 capped so that one slab [T_pad][width] and one head chunk
+ *                 [width][d_i] stay below 4 GiB (T_pad = T rounded up to 128).
+ *                 A backward whose T_pad * d_i bf16 panel would reach 4 GiB
+ *                 runs on the general (slower) kernels instead.
  */
 typedef struct mls_problem {
   int32_t M;

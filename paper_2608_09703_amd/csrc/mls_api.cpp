@@ -98,6 +98,11 @@ struct Plan {
   int n_vt_fwd = 0;
   int64_t Vc = 0;
   int n_chunks = 0;
+  // The wide gradient GEMM addresses its M-contiguous operands (the slab,
+  // h_i, the head chunk) with 32-bit offsets over the whole K extent, so each
+  // must stay below 4 GiB; a backward where h_i alone would not takes the
+  // general path, which addresses with 64 bits.
+  bool wide_bwd = false;
   // forward workspace
   size_t off_partials = 0, off_lab = 0, fwd_bytes = 0;
   // backward workspace
@@ -155,6 +160,10 @@ void make_plan(const mls_problem* p, Plan& pl) {
   pl.n_tt = (int)(pl.T_pad / kFusedBN);
   const int fbm = fused_tile_rows(pl.wide);
   pl.n_vt_fwd = (int)((p->V + fbm - 1) / fbm);
+  constexpr int64_t kPanelMax = (1ll << 32) - 1;  // bytes one wide-GEMM operand may span
+  int64_t dmax = 0;
+  for (int i = 0; i < p->M; ++i) dmax = std::max<int64_t>(dmax, p->d[i]);
+  pl.wide_bwd = pl.wide && pl.T_pad * dmax * pl.es <= kPanelMax && pl.T_pad * 256 * pl.es <= kPanelMax;
   const int64_t vmax = round_up(p->V, 256);
   int64_t vc;
   if (p->vocab_chunk > 0) {
@@ -164,10 +173,15 @@ void make_plan(const mls_problem* p, Plan& pl) {
     // would exceed kSlabTargetBytes (the wide path keeps one slab layout, the
     // general path two), so the logit-gradient slab never spans the whole
     // vocabulary (V > 256).
-    const int64_t per_row = (pl.wide ? 1ll : 2ll) * pl.M * pl.T_pad * pl.es;
+    const int64_t per_row = (pl.wide_bwd ? 1ll : 2ll) * pl.M * pl.T_pad * pl.es;
     const int64_t fit = std::max<int64_t>(256, kSlabTargetBytes / per_row / 256 * 256);
     const int64_t n = std::max<int64_t>(kMinChunks, (p->V + fit - 1) / fit);
     vc = round_up((p->V + n - 1) / n, 256);
+  }
+  if (pl.wide_bwd) {
+    // one slab [T_pad][Vc] and one head chunk [Vc][d_i] below 4 GiB each
+    const int64_t cap = std::min(kPanelMax / (pl.T_pad * pl.es), kPanelMax / (dmax * pl.es)) / 256 * 256;
+    vc = std::min(vc, cap);
   }
   pl.Vc = std::max<int64_t>(256, std::min(vc, vmax));
   pl.n_chunks = (int)((p->V + pl.Vc - 1) / pl.Vc);
@@ -183,7 +197,7 @@ void make_plan(const mls_problem* p, Plan& pl) {
   const size_t slab = (size_t)pl.M * pl.T_pad * pl.Vc * pl.es;
   pl.off_slab = off;
   off = align256(off + slab);
-  if (!pl.wide) {  // general path: G^T slab and transposed operands as well
+  if (!pl.wide_bwd) {  // general path: G^T slab and transposed operands as well
     pl.off_slabT = off;
     off = align256(off + slab);
     pl.off_hT = off;
@@ -424,7 +438,8 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
 
   FusedArgs a;
   fill_common(p, pl, a);
-  a.n_vt = (int)(pl.Vc / fused_tile_rows(pl.wide));
+  a.wide = pl.wide_bwd ? 1 : 0;
+  a.n_vt = (int)(pl.Vc / fused_tile_rows(pl.wide_bwd));
   a.lse1 = sf;
   a.lset = sf + (int64_t)pl.M * pl.T;
   a.n_valid = reinterpret_cast<const int32_t*>(static_cast<const char*>(stats) + pl.header_off);
@@ -432,7 +447,7 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
   a.g_kl = g_kl;
   host_coeffs(pl.M, pl.s, p->alpha, p->tau, MLS_MODE_PAPER, nullptr, a.host_gce, a.host_gkl);
   a.slab = ws + pl.off_slab;
-  a.slabT = pl.wide ? nullptr : ws + pl.off_slabT;
+  a.slabT = pl.wide_bwd ? nullptr : ws + pl.off_slabT;
   char* hT = ws + pl.off_hT;
   char* WT = ws + pl.off_WT;
 
@@ -443,12 +458,12 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
     acc += p->d[i];
   }
   const size_t slab_stride = (size_t)pl.T_pad * pl.Vc * pl.es;
-  const int tbm = gemm_tile_rows(pl.wide);
-  const int tbn = gemm_tile_cols(pl.wide);
+  const int tbm = gemm_tile_rows(pl.wide_bwd);
+  const int tbn = gemm_tile_cols(pl.wide_bwd);
   hipError_t e;
 
   // general path: h_i^T [d_i, T_pad] for the grad_W products
-  if (!pl.wide) {
+  if (!pl.wide_bwd) {
     TransposeArgs ta;
     memset(&ta, 0, sizeof(ta));
     int64_t maxc = 0;
@@ -477,7 +492,7 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
     const int64_t vrows = std::min(pl.Vc, pl.V - v0);
 
     // general path: W_i[chunk]^T [d_i, Vc] for the grad_h products
-    if (!pl.wide) {
+    if (!pl.wide_bwd) {
     TransposeArgs ta;
     memset(&ta, 0, sizeof(ta));
     int64_t maxc = 0;
@@ -502,7 +517,7 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
     }
 
     a.v0 = v0;
-    if (pl.wide) {
+    if (pl.wide_bwd) {
       // The wide GEMM reads slab columns past the chunk's rows only up to the
       // K-tile holding its last row (grad_h) or for output rows it does not
       // store (grad_W), so the vocabulary tiles past the chunk end are skipped.
@@ -528,7 +543,7 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
       g.A = static_cast<const char*>(a.slab) + (size_t)i * slab_stride;
       g.lda = pl.Vc;
       g.rows = pl.T;
-      if (pl.wide) {
+      if (pl.wide_bwd) {
         g.B = static_cast<const char*>(p->W[i]) + (size_t)v0 * p->d[i] * pl.es;  // [v][d]
         g.ldb = p->d[i];
         g.cols = vrows;
@@ -543,7 +558,7 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
       // the chunk's rows past vrows read as zero from the head: the last,
       // shorter chunk stops at the K-tile holding its last row
       const int64_t kt = gemm_wide_k_tile();
-      g.K = pl.wide ? std::min(pl.Vc, (vrows + kt - 1) / kt * kt) : pl.Vc;
+      g.K = pl.wide_bwd ? std::min(pl.Vc, (vrows + kt - 1) / kt * kt) : pl.Vc;
       g.kind = 0;
       g.tiles_m = (int)((pl.T + tbm - 1) / tbm);
       g.tiles_n = (int)((p->d[i] + tbn - 1) / tbn);
@@ -556,7 +571,7 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
     for (int i = 0; i < pl.M; ++i) {
       if (!grad_W[i]) continue;
       GemmGroup& g = ga.g[ga.ngroups++];
-      if (pl.wide) {
+      if (pl.wide_bwd) {
         g.A = static_cast<const char*>(a.slab) + (size_t)i * slab_stride;  // [t][v]
         g.lda = pl.Vc;
         g.rows = pl.T_pad;
@@ -596,7 +611,7 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
     }
     {
       ProfScope ps("gemm_grads", s);
-      e = pl.wide ? launch_gemm_wide(ga, tiles, s) : launch_gemm_nt(ga, tiles, pl.f32, s);
+      e = pl.wide_bwd ? launch_gemm_wide(ga, tiles, s) : launch_gemm_nt(ga, tiles, pl.f32, s);
     }
     if (e != hipSuccess) return hip_fail(e, "gradient GEMM launch");
   }

@@ -95,6 +95,25 @@ def test_query_sizes_reports_workspace_and_stats():
     assert B.query_sizes(p1)[0] >= M * T * 50304 * 2
 
 
+
+def test_wide_backward_operands_stay_below_4_gib():
+    """The wide gradient GEMM addresses each M-contiguous operand with 32-bit
+    offsets: the chunk width is capped so one [T_pad][V_c] slab stays below 4 GiB,
+    and a T x d_i panel that would reach 4 GiB sends the backward to the general
+    kernels (which then also keep transposed copies of h_i)."""
+    T, V = 1 << 22, 4096
+    # explicit whole-vocabulary chunk: an uncapped slab would take T * V * 2 = 32 GiB
+    ws_wide, _ = B.query_sizes(_fake_problem(M=1, dims=[64], T=T, V=V, vocab_chunk=V))
+    assert ws_wide < (1 << 32)
+    # widths that are not multiples of 64 take the general kernels: no cap there
+    ws_gen, _ = B.query_sizes(_fake_problem(M=1, dims=[72], T=T, V=V, vocab_chunk=V))
+    assert ws_gen >= 2 * T * V * 2
+    # T * d * 2 = 8 GiB: general backward, whose h^T copy alone takes 8 GiB
+    ws_big, _ = B.query_sizes(_fake_problem(M=1, dims=[1024], T=T, V=V))
+    assert ws_big >= T * 1024 * 2
+    ws_small, _ = B.query_sizes(_fake_problem(M=1, dims=[256], T=T, V=V))
+    assert ws_small < T * 256 * 2 * 4
+
 @pytest.mark.parametrize("field,value,status", [
     ("M", 0, B.MLS_INVALID_ARG),
     ("M", 9, B.MLS_INVALID_ARG),
