@@ -649,7 +649,7 @@ mls_status mls_diagnostics(const mls_problem* p, float* kl_pair, float* agree, i
   a.ignore_index = p->ignore_index;
   a.n_tt = pl.n_tt_diag;
   a.n_vt = pl.n_vt_diag;
-  a.group_v = 8;
+  a.group_v = 4;  // measured: 4 > 8 > 16 here (8 for the forward and backward)
   a.partials = reinterpret_cast<float*>(ws + pl.off_dpart);
   a.rowvals = reinterpret_cast<float*>(ws + pl.off_drow);
   a.kl_pair = kl_pair;
