@@ -249,7 +249,9 @@ void fill_common(const mls_problem* p, const Plan& pl, FusedArgs& a) {
   a.tau = p->tau;
   a.inv_tau = 1.0f / p->tau;
   a.wide = pl.wide ? 1 : 0;
-  a.group_v = 8;
+  // vocabulary tiles per group of the tile order: measured best at 8 for
+  // T <= 4096 and at 4 from T = 8192 on (C3-C5 shapes)
+  a.group_v = pl.n_tt >= 64 ? 4 : 8;
   a.n_tt = pl.n_tt;
   a.T_pad = pl.T_pad;
   a.Vc = pl.Vc;
