@@ -122,8 +122,13 @@ __device__ __forceinline__ uint2 lds_read_tr8(const char* p) {
   return __builtin_bit_cast(uint2, v);
 }
 
+// SPREAD: the next K-tile's loads are issued a few at a time across the K-steps
+// of the current one instead of in one burst after the barrier, so their LDS
+// writes interleave with the fragment reads. It pays where a K-tile lasts long
+// enough to cover the load latency from its last K-step (the 256 x 256 GEMM
+// tile), and costs where it does not (the 128 x 128 fused tiles).
 template <int BM, int BN, int WGM, int WGN, int STAGES, int RB = 128, int ALAY = kLayoutKC,
-          int BLAY = kLayoutKC>
+          int BLAY = kLayoutKC, bool SPREAD = false>
 struct WideMma {
   static constexpr int kBM = BM;
   static constexpr int kBN = BN;
@@ -226,6 +231,26 @@ struct WideMma {
     }
   }
 
+  // Issues load j (0 .. LA + LB - 1) of one K-tile into stage `st`; ka / kb
+  // are the tile's K positions as issue_operand takes them.
+  __device__ __forceinline__ static void issue_one(int j, __amdgpu_buffer_rsrc_t ra,
+                                                   __amdgpu_buffer_rsrc_t rb, const uint32_t* offa,
+                                                   const uint32_t* offb, uint32_t ka, uint32_t kb,
+                                                   char* st, int wave) {
+    if (j < LA) {
+      char* dst = st + (j * NW + wave) * 64 * 16;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void_t*)dst, 16,
+                                               offa[j] + (ALAY == kLayoutKC ? 0u : ka),
+                                               ALAY == kLayoutKC ? (int)ka : 0, 0, 0);
+    } else {
+      const int jb = j - LA;
+      char* dst = st + BM * RB + (jb * NW + wave) * 64 * 16;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void_t*)dst, 16,
+                                               offb[jb] + (BLAY == kLayoutKC ? 0u : kb),
+                                               BLAY == kLayoutKC ? (int)kb : 0, 0, 0);
+    }
+  }
+
   // One MFMA operand fragment of an MC tile: row block `r0` (32 rows), K-step kk.
   template <int ROWS>
   __device__ __forceinline__ static uint4 mc_frag(const char* base, int r0, int kk, int lane) {
@@ -260,8 +285,10 @@ struct WideMma {
     }
   }
 
+  // `hook(kk)` runs at the start of K-step kk (the spread loads of the next K-tile).
+  template <class Hook>
   __device__ __forceinline__ void compute_stage(const char* sA, const char* sB, int lane, int wm,
-                                                int wn) {
+                                                int wn, Hook&& hook) {
     constexpr int kMfma = FM * FN;
     constexpr int kReads = (FM + FN) * ((ALAY == kLayoutMC || BLAY == kLayoutMC) ? 2 : 1);
     constexpr int kPer = kMfma / kReads > 0 ? kMfma / kReads : 1;  // MFMAs per read
@@ -270,6 +297,10 @@ struct WideMma {
 #pragma unroll
     for (int kk = 0; kk < KSTEPS; ++kk) {
       __builtin_amdgcn_sched_barrier(0);
+      if constexpr (SPREAD) {
+        hook(kk);
+        __builtin_amdgcn_sched_barrier(0);
+      }
       if (kk < KSTEPS - 1) load_frags(sA, sB, kk + 1, lane, wm, wn, a[(kk + 1) & 1], b[(kk + 1) & 1]);
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
@@ -349,16 +380,31 @@ struct WideMma {
       // have completed
       stage_barrier();
       const int nt = kt + STAGES - 1;
-      if (nt < nk) {
+      const char* stage = smem + (kt % STAGES) * kStageBytes;
+      if constexpr (!SPREAD) {
+        if (nt < nk) {
+          char* st = smem + (nt % STAGES) * kStageBytes;
+          const uint32_t ka = nt * stepa, kb = nt * stepb;
+          issue_operand<LA>(ra, offa, ALAY == kLayoutKC ? 0u : ka, ALAY == kLayoutKC ? (int)ka : 0,
+                            st, wave);
+          issue_operand<LB>(rb, offb, BLAY == kLayoutKC ? 0u : kb, BLAY == kLayoutKC ? (int)kb : 0,
+                            st + BM * RB, wave);
+        }
+        compute_stage(stage, stage + BM * RB, lane, wm, wn, [](int) {});
+      } else {
         char* st = smem + (nt % STAGES) * kStageBytes;
         const uint32_t ka = nt * stepa, kb = nt * stepb;
-        issue_operand<LA>(ra, offa, ALAY == kLayoutKC ? 0u : ka, ALAY == kLayoutKC ? (int)ka : 0, st,
-                          wave);
-        issue_operand<LB>(rb, offb, BLAY == kLayoutKC ? 0u : kb, BLAY == kLayoutKC ? (int)kb : 0,
-                          st + BM * RB, wave);
+        const bool more = nt < nk;
+        compute_stage(stage, stage + BM * RB, lane, wm, wn, [&](int kk) {
+          if (!more) return;
+          constexpr int kPerStep = (kLoadsPerTile + KSTEPS - 1) / KSTEPS;
+#pragma unroll
+          for (int q = 0; q < kPerStep; ++q) {
+            const int j = kk * kPerStep + q;
+            if (j < kLoadsPerTile) issue_one(j, ra, rb, offa, offb, ka, kb, st, wave);
+          }
+        });
       }
-      const char* stage = smem + (kt % STAGES) * kStageBytes;
-      compute_stage(stage, stage + BM * RB, lane, wm, wn);
     }
     stage_barrier();
   }

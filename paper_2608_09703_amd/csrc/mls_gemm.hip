@@ -59,13 +59,13 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_nt_kernel(GemmArgs a) {
 
 // bf16 path: 256 x 256 tiles, 8 waves (2 per SIMD), direct-to-LDS loads, 2
 // stages of 64-wide K (each K-tile reads whole 128-byte lines of a K-contiguous
-// operand). The head chunk (grad_h) and the slab and h (grad_W) are
+// operand); the next K-tile's loads are spread over the current one's K-steps. The head chunk (grad_h) and the slab and h (grad_W) are
 // read in their stored layouts through transposing LDS reads, so no operand is
 // ever transposed in memory.
 constexpr int kWideBM = 256;
 constexpr int kWideBN = 256;
-using WideGemmH = WideMma<kWideBM, kWideBN, 2, 4, 2, 128, kLayoutKC, kLayoutMC>;
-using WideGemmW = WideMma<kWideBM, kWideBN, 2, 4, 2, 128, kLayoutMC, kLayoutMC>;
+using WideGemmH = WideMma<kWideBM, kWideBN, 2, 4, 2, 128, kLayoutKC, kLayoutMC, true>;
+using WideGemmW = WideMma<kWideBM, kWideBN, 2, 4, 2, 128, kLayoutMC, kLayoutMC, true>;
 
 template <class Mma>
 __device__ __forceinline__ void wide_tile(const GemmGroup& g, int tm, int tn, int64_t mext,
