@@ -210,7 +210,7 @@ void make_plan(const mls_problem* p, Plan& pl) {
   // diagnostics: one record per (vocabulary tile, token)
   if (pl.M <= kMaxDiagModels) {
     pl.n_vt_diag = (int)((p->V + diag_tile_rows(pl.wide) - 1) / diag_tile_rows(pl.wide));
-    pl.n_tt_diag = (int)((p->T + diag_tile_cols(pl.wide) - 1) / diag_tile_cols(pl.wide));
+    pl.n_tt_diag = (int)((p->T + diag_tile_cols(pl.wide, pl.M) - 1) / diag_tile_cols(pl.wide, pl.M));
     off = 0;
     pl.off_dpart = off;
     off = align256(off + (size_t)pl.n_vt_diag * pl.T * diag_record_floats(pl.M) * sizeof(float));

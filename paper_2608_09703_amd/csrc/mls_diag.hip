@@ -323,11 +323,12 @@ __global__ __launch_bounds__(kRedThreads) void diag_mean_kernel(DiagArgs a) {
 
 // All M accumulator sets of a tile stay live. Up to M = 3 the wide bf16 path
 // runs four waves of 64x64 (64 accumulators per lane per model) at two blocks
-// per CU; for M = 4 that no longer fits, and eight waves of 64x32 (32 per
-// model) share the 128x128 tile. The general path uses the four-wave
-// register-staged core on 128x64.
+// per CU; for M = 4 that no longer fits, and four waves of 64x32 (32 per
+// model) take a 128x64 tile, still two blocks per CU (two independent blocks
+// hide each other's barriers better than one eight-wave block on 128x128).
+// The general path uses the four-wave register-staged core on 128x64.
 using DiagWide = WideMma<kFusedWideBM, kDiagBN, 2, 2, 2>;
-using DiagWide8 = WideMma<kFusedWideBM, kDiagBN, 2, 4, 2>;
+using DiagWide4 = WideMma<kFusedWideBM, kDiagBN / 2, 2, 2, 2>;
 template <typename E>
 using DiagGen = TileMma<E, kFusedBM, kDiagGenBN, 2, 2>;
 
@@ -342,7 +343,7 @@ hipError_t launch_tiles_m(const DiagArgs& a, bool f32, bool wide, hipStream_t st
       hipLaunchKernelGGL((diag_tile_kernel<DiagWide, Bf16, MM, 2>), grid, dim3(DiagWide::NT), 0,
                          stream, a);
     else
-      hipLaunchKernelGGL((diag_tile_kernel<DiagWide8, Bf16, MM, 1>), grid, dim3(DiagWide8::NT), 0,
+      hipLaunchKernelGGL((diag_tile_kernel<DiagWide4, Bf16, MM, 2>), grid, dim3(DiagWide4::NT), 0,
                          stream, a);
   }
   else
@@ -364,7 +365,7 @@ hipError_t launch_reduce_m(const DiagArgs& a, hipStream_t stream) {
 }  // namespace
 
 int diag_tile_rows(bool wide) { return wide ? kFusedWideBM : kFusedBM; }
-int diag_tile_cols(bool wide) { return wide ? kDiagBN : kDiagGenBN; }
+int diag_tile_cols(bool wide, int M) { return wide ? (M == 4 ? kDiagBN / 2 : kDiagBN) : kDiagGenBN; }
 int diag_record_floats(int M) { return M * M + 3 * M; }
 
 hipError_t launch_diag_tiles(const DiagArgs& a, bool f32, bool wide, hipStream_t stream) {

@@ -244,7 +244,7 @@ hipError_t launch_transpose(const TransposeArgs& a, int64_t max_out_rows, int64_
                             bool f32, hipStream_t stream);
 int gemm_wide_k_tile();  // K values per K-tile of the wide gradient GEMM
 int diag_tile_rows(bool wide);
-int diag_tile_cols(bool wide);
+int diag_tile_cols(bool wide, int M);
 int diag_record_floats(int M);
 hipError_t launch_diag_tiles(const DiagArgs& a, bool f32, bool wide, hipStream_t stream);
 hipError_t launch_diag_reduce(const DiagArgs& a, hipStream_t stream);
