@@ -209,7 +209,7 @@ __global__ __launch_bounds__(Mma::NT, MINB) void diag_tile_kernel(DiagArgs a) {
 // block takes kRowTok tokens; its kRowSlices thread rows each merge every
 // kRowSlices-th vocabulary tile, and the slices are merged in a fixed order.
 constexpr int kRowTok = 32;
-constexpr int kRowSlices = 8;
+constexpr int kRowSlices = 16;
 
 template <int MM>
 __global__ __launch_bounds__(kRowTok * kRowSlices) void diag_rows_kernel(DiagArgs a) {
