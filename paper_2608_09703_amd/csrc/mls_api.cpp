@@ -188,7 +188,7 @@ void make_plan(const mls_problem* p, Plan& pl) {
 
   size_t off = 0;
   pl.off_partials = off;
-  off = align256(off + (size_t)pl.M * pl.n_vt_fwd * pl.T * sizeof(float4));
+  off = align256(off + (size_t)pl.M * pl.n_vt_fwd * kFusedFwdParts * pl.T_pad * sizeof(float4));
   pl.off_lab = off;
   off = align256(off + (size_t)pl.M * pl.T * sizeof(float));
   pl.fwd_bytes = off;
@@ -271,7 +271,8 @@ void fill_rows(const mls_problem* p, const Plan& pl, RowArgs& r) {
   r.labels = p->labels;
   r.ignore_index = p->ignore_index;
   r.tau = p->tau;
-  r.n_vt = pl.n_vt_fwd;
+  r.n_rec = pl.n_vt_fwd * kFusedFwdParts;
+  fill_order(pl, r.order);
 }
 
 void host_coeffs(int M, int s, float alpha, float tau, int mode, const float* w, float* g_ce,

@@ -7,8 +7,9 @@
 // student's). The teacher's tile is computed first and its exponentials
 // e_v = exp((l_s,v - max) / tau) stay in registers, laid out exactly like the
 // accumulators of the students' tiles, so each student adds its cross term
-// sum_v e_v l_i,v with no extra memory traffic. Only per-tile partial rows
-// (max, sum exp, sum exp / tau, cross term) leave the block.
+// sum_v e_v l_i,v with no extra memory traffic. Only partial rows (max, sum
+// exp, sum exp / tau, cross term), one per wave row of the tile, leave the
+// block.
 //
 // Backward (per vocabulary chunk): logits are recomputed tile by tile, the
 // teacher's q = softmax(l_s / tau) is formed once per tile and reused by every
@@ -61,6 +62,11 @@ struct TeacherTile<FM, FN, true> {
   }
 };
 
+// Forward tile kernel: for each sub-model (the teacher first) the logit tile
+// of BM vocabulary rows x BN tokens, reduced in registers to one partial record
+// (max, sum exp, sum exp at tau, teacher-weighted logit sum) per token and wave
+// row. Each wave normalises to the max over its own rows, so the epilogue needs
+// no exchange between waves; the row merge rescales the records.
 template <class Mma, typename E, bool TAU1, int MINB = 1>
 __global__ __launch_bounds__(Mma::NT, MINB) void fused_fwd_kernel(FusedArgs a) {
   constexpr int BM = Mma::kBM;
@@ -68,8 +74,9 @@ __global__ __launch_bounds__(Mma::NT, MINB) void fused_fwd_kernel(FusedArgs a) {
   constexpr int WGM = Mma::kWGM;
   constexpr int FM = Mma::FM;
   constexpr int FN = Mma::FN;
+  static_assert(WGM == kFusedFwdParts, "one partial record per wave row");
+  static_assert(BN == kFusedBN, "partial records are grouped by token tile");
   __shared__ __attribute__((aligned(16))) char smem[Mma::kSmemBytes];
-  __shared__ float red[WGM][BN][4];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -84,6 +91,9 @@ __global__ __launch_bounds__(Mma::NT, MINB) void fused_fwd_kernel(FusedArgs a) {
   const int64_t tbase = (int64_t)tt * BN;
   const bool full = vbase + BM <= a.V;
   const float ct = kLog2e * a.inv_tau;
+  // records of sub-model order[oi] and token tile tt: [n_vt * WGM][BN]
+  const int64_t n_rec = (int64_t)a.n_vt * WGM;
+  const int64_t rec = (int64_t)vt * WGM + wm;
 
   // teacher weights exp((l_s - max_s) / tau); 0 outside V
   TeacherTile<FM, FN, false> e_t;
@@ -95,34 +105,21 @@ __global__ __launch_bounds__(Mma::NT, MINB) void fused_fwd_kernel(FusedArgs a) {
     mma.run(static_cast<const char*>(a.W[i]), kb, vbase, a.V, static_cast<const char*>(a.h[i]),
             kb, tbase, a.T, kb, smem, tid);
 
-    // 1. block max of each token column over the tile's valid vocabulary rows
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) {
-      float m = -INFINITY;
+      // 1. max of the token column over the wave's valid vocabulary rows
+      // (-inf when all of them lie beyond V)
+      float mb = -INFINITY;
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const bool ok = full || vbase + Mma::row_of(wm, fm, r, lane) < a.V;
-          if (ok) m = fmaxf(m, mma.acc[fm][fn][r]);
+          if (ok) mb = fmaxf(mb, mma.acc[fm][fn][r]);
         }
-      m = fmaxf(m, shfl_xor32(m));
-      if (hi == 0) red[wm][Mma::col_of(wn, fn, lane)][0] = m;
-    }
-    __syncthreads();
-    float mb[FN];
-#pragma unroll
-    for (int fn = 0; fn < FN; ++fn) {
-      const int c = Mma::col_of(wn, fn, lane);
-      float m = red[0][c][0];
-#pragma unroll
-      for (int w = 1; w < WGM; ++w) m = fmaxf(m, red[w][c][0]);
-      mb[fn] = m;
-    }
+      mb = fmaxf(mb, shfl_xor32(mb));
 
-    // 2. sums relative to the block max
-#pragma unroll
-    for (int fn = 0; fn < FN; ++fn) {
+      // 2. sums relative to that max (every term is 0 on rows beyond V)
       float s1 = 0.f, st = 0.f, xr = 0.f;
       if (oi == 0) {
 #pragma unroll
@@ -131,7 +128,7 @@ __global__ __launch_bounds__(Mma::NT, MINB) void fused_fwd_kernel(FusedArgs a) {
           for (int r = 0; r < 16; ++r) {
             const bool ok = full || vbase + Mma::row_of(wm, fm, r, lane) < a.V;
             const float l = mma.acc[fm][fn][r];
-            const float x = l - mb[fn];
+            const float x = l - mb;
             const float e = ok ? fast_exp2(x * ct) : 0.f;
             e_t.set(fm, fn, r, e);
             st += e;
@@ -146,7 +143,7 @@ __global__ __launch_bounds__(Mma::NT, MINB) void fused_fwd_kernel(FusedArgs a) {
           for (int r = 0; r < 16; ++r) {
             const bool ok = full || vbase + Mma::row_of(wm, fm, r, lane) < a.V;
             const float l = mma.acc[fm][fn][r];
-            const float x = l - mb[fn];
+            const float x = l - mb;
             s1 += ok ? fast_exp2(x * kLog2e) : 0.f;
             if (!TAU1) st += ok ? fast_exp2(x * ct) : 0.f;
             xr = fmaf(e_t.get(fm, fn, r), l, xr);
@@ -156,31 +153,12 @@ __global__ __launch_bounds__(Mma::NT, MINB) void fused_fwd_kernel(FusedArgs a) {
       s1 += shfl_xor32(s1);
       st += shfl_xor32(st);
       xr += shfl_xor32(xr);
-      if (hi == 0) {
-        const int c = Mma::col_of(wn, fn, lane);
-        red[wm][c][1] = s1;
-        red[wm][c][2] = st;
-        red[wm][c][3] = xr;
-      }
-    }
-    __syncthreads();
 
-    // 3. one partial row per token
-    if (tid < BN) {
-      const int64_t t = tbase + tid;
-      if (t < a.T) {
-        float m = red[0][tid][0], s1 = red[0][tid][1], st = red[0][tid][2], xr = red[0][tid][3];
-#pragma unroll
-        for (int w = 1; w < WGM; ++w) {
-          m = fmaxf(m, red[w][tid][0]);
-          s1 += red[w][tid][1];
-          st += red[w][tid][2];
-          xr += red[w][tid][3];
-        }
-        a.partials[((int64_t)i * a.n_vt + vt) * a.T + t] = make_float4(m, s1, st, xr);
-      }
+      // 3. the wave's partial record of this token
+      const int c = Mma::col_of(wn, fn, lane);
+      if (hi == 0 && tbase + c < a.T)
+        a.partials[(((int64_t)oi * a.n_tt + tt) * n_rec + rec) * BN + c] = make_float4(mb, s1, st, xr);
     }
-    // `red` is rewritten only after the next tile product, which synchronises.
   }
 }
 

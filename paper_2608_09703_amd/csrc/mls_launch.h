@@ -14,6 +14,9 @@ constexpr int kMaxModels = 8;
 // Tile of the fused logits kernels: BM vocabulary rows x BN token columns.
 constexpr int kFusedBM = 128;      // general core
 constexpr int kFusedWideBM = 128;  // wide bf16 core (all widths multiples of 64)
+// forward partial records per (vocabulary tile, token, sub-model): one per
+// wave row of the tile, each over its own half of the tile's rows
+constexpr int kFusedFwdParts = 2;
 constexpr int kFusedBN = 128;
 // Tile of the backward GEMMs.
 constexpr int kGemmBM = 128;
@@ -44,7 +47,7 @@ struct FusedArgs {
   int32_t n_tt;  // token tiles
   int32_t n_vt;  // vocabulary tiles in this launch
   // forward
-  float4* partials;  // [M][n_vt][T]
+  float4* partials;  // [M (processing order)][n_tt][n_vt * kFusedFwdParts][kFusedBN]
   // backward
   const float* lse1;  // [M][T]
   const float* lset;  // [M][T]
@@ -123,8 +126,9 @@ struct RowArgs {
   const int64_t* labels;
   int64_t ignore_index;
   float tau;
-  int32_t n_vt;
-  const float4* partials;  // [M][n_vt][T]
+  int32_t order[kMaxModels];  // sub-model of each partial slot; order[0] is the teacher
+  int32_t n_rec;           // partial records per token and sub-model
+  const float4* partials;  // [M slots][ceil(T / kFusedBN)][n_rec][kFusedBN]
   float* lab;              // [M][T] label logits
   float* stats;            // lse1, lset, ce_row, kl_row, h_row
   int32_t* header;         // n_valid, flags

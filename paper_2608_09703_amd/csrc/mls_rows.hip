@@ -53,117 +53,110 @@ __global__ __launch_bounds__(kThreads) void label_logits_kernel(RowArgs a) {
 // Running merge of partial rows. Every sub-model keeps its own max m,
 // sum exp(l - m) (s1) and sum exp((l - m) / tau) (st); the cross terms xr of
 // every sub-model are weighted by the teacher's exponentials, so they are
-// rescaled with the teacher's max.
+// rescaled with the teacher's max. Slots follow the processing order, slot 0
+// being the teacher; MM (the number of sub-models) is a compile-time constant,
+// so every array is indexed with constants and stays in registers.
+template <int MM>
 struct RowState {
-  float m[kMaxModels];
-  float s1[kMaxModels];
-  float st[kMaxModels];
-  float xr[kMaxModels];
+  float m[MM];
+  float s1[MM];
+  float st[MM];
+  float xr[MM];
 };
 
-// arr[s] for a runtime s, with compile-time indices (keeps arr in registers)
-template <typename X>
-__device__ __forceinline__ X pick(const X* arr, int s) {
-  X r = arr[0];
+// rec[k] = partial of slot k over one vocabulary range (the same for all k)
+template <int MM>
+__device__ __forceinline__ void absorb(RowState<MM>& st, float ct, const float4* rec) {
+  const float ms_new = fmaxf(st.m[0], rec[0].x);
+  const float wa = fast_exp2((st.m[0] - ms_new) * ct);
+  const float wb = fast_exp2((rec[0].x - ms_new) * ct);
 #pragma unroll
-  for (int i = 1; i < kMaxModels; ++i)
-    if (i == s) r = arr[i];
-  return r;
-}
-
-__device__ __forceinline__ void absorb(RowState& st, int M, int s, float ct, const float4* rec) {
-  // rec[i] = partial of sub-model i (same vocabulary range for all i). The
-  // teacher's entries are picked with compile-time indices so that rec and st
-  // stay in registers.
-  float ms_old = 0.f, rs_x = 0.f;
-#pragma unroll
-  for (int i = 0; i < kMaxModels; ++i)
-    if (i == s) {
-      ms_old = st.m[i];
-      rs_x = rec[i].x;
-    }
-  const float ms_new = fmaxf(ms_old, rs_x);
-  const float wa = fast_exp2((ms_old - ms_new) * ct);
-  const float wb = fast_exp2((rs_x - ms_new) * ct);
-#pragma unroll
-  for (int i = 0; i < kMaxModels; ++i) {
-    if (i >= M) continue;  // (not break: keeps the loop fully unrolled)
-    const float mo = st.m[i];
-    const float mn = fmaxf(mo, rec[i].x);
-    st.s1[i] = st.s1[i] * fast_exp2((mo - mn) * kLog2e) + rec[i].y * fast_exp2((rec[i].x - mn) * kLog2e);
-    st.st[i] = st.st[i] * fast_exp2((mo - mn) * ct) + rec[i].z * fast_exp2((rec[i].x - mn) * ct);
-    st.xr[i] = st.xr[i] * wa + rec[i].w * wb;
-    st.m[i] = mn;
+  for (int k = 0; k < MM; ++k) {
+    const float mo = st.m[k];
+    const float mn = fmaxf(mo, rec[k].x);
+    st.s1[k] = st.s1[k] * fast_exp2((mo - mn) * kLog2e) + rec[k].y * fast_exp2((rec[k].x - mn) * kLog2e);
+    st.st[k] = st.st[k] * fast_exp2((mo - mn) * ct) + rec[k].z * fast_exp2((rec[k].x - mn) * ct);
+    st.xr[k] = st.xr[k] * wa + rec[k].w * wb;
+    st.m[k] = mn;
   }
 }
 
 constexpr int kRowTok = 16;   // tokens per block
-constexpr int kRowGrp = 16;   // partial groups per token (merged in a fixed order)
+constexpr int kRowGrp = 16;   // partial groups per token, merged pairwise in a fixed tree
+static_assert(kRowTok * kRowGrp == kThreads && (kRowGrp & (kRowGrp - 1)) == 0, "row merge shape");
+static_assert(kFusedBN % kRowTok == 0, "a block's tokens lie in one token tile");
 
+template <int MM>
 __global__ __launch_bounds__(kThreads) void finalize_rows_kernel(RowArgs a) {
-  __shared__ float4 sh[kRowGrp - 1][kRowTok][kMaxModels];
+  __shared__ float4 sh[kRowGrp][kRowTok][MM];
   const int tl = threadIdx.x % kRowTok;
   const int grp = threadIdx.x / kRowTok;
   const int64_t t = (int64_t)blockIdx.x * kRowTok + tl;
-  const int M = a.M;
-  const int s = a.teacher;
   const float inv_tau = 1.0f / a.tau;
   const float ct = kLog2e * inv_tau;
 
-  RowState st;
+  RowState<MM> st;
 #pragma unroll
-  for (int i = 0; i < kMaxModels; ++i) {
+  for (int i = 0; i < MM; ++i) {
     st.m[i] = -INFINITY;
     st.s1[i] = 0.f;
     st.st[i] = 0.f;
     st.xr[i] = 0.f;
   }
+  const int64_t n_tt = (a.T + kFusedBN - 1) / kFusedBN;
+  const float4* part = a.partials + (t / kFusedBN) * a.n_rec * kFusedBN + t % kFusedBN;
   if (t < a.T) {
 #pragma unroll 4
-    for (int j = grp; j < a.n_vt; j += kRowGrp) {
-      float4 rec[kMaxModels];
+    for (int j = grp; j < a.n_rec; j += kRowGrp) {
+      float4 rec[MM];
 #pragma unroll
-      for (int i = 0; i < kMaxModels; ++i)
-        if (i < M) rec[i] = a.partials[((int64_t)i * a.n_vt + j) * a.T + t];
-      absorb(st, M, s, ct, rec);
+      for (int k = 0; k < MM; ++k) rec[k] = part[((int64_t)k * n_tt * a.n_rec + j) * kFusedBN];
+      if (rec[0].x != -INFINITY) absorb<MM>(st, ct, rec);  // else rows all beyond V
     }
   }
-  if (grp > 0) {
+  // group g absorbs group g + w for w = kRowGrp / 2, ..., 1 (every thread
+  // takes part in the barriers; columns past T only merge among themselves)
 #pragma unroll
-    for (int i = 0; i < kMaxModels; ++i)
-      if (i < M) sh[grp - 1][tl][i] = make_float4(st.m[i], st.s1[i], st.st[i], st.xr[i]);
+  for (int i = 0; i < MM; ++i) sh[grp][tl][i] = make_float4(st.m[i], st.s1[i], st.st[i], st.xr[i]);
+#pragma unroll
+  for (int w = kRowGrp / 2; w >= 1; w >>= 1) {
+    __syncthreads();
+    if (grp < w) {
+      float4 rec[MM];
+#pragma unroll
+      for (int i = 0; i < MM; ++i) rec[i] = sh[grp + w][tl][i];
+      if (rec[0].x != -INFINITY) {  // else that group saw no record
+        absorb<MM>(st, ct, rec);
+        if (w > 1) {
+#pragma unroll
+          for (int i = 0; i < MM; ++i)
+            sh[grp][tl][i] = make_float4(st.m[i], st.s1[i], st.st[i], st.xr[i]);
+        }
+      }
+    }
   }
-  __syncthreads();
   if (grp != 0 || t >= a.T) return;
-  for (int g2 = 0; g2 < kRowGrp - 1; ++g2) {
-    float4 rec[kMaxModels];
-#pragma unroll
-    for (int i = 0; i < kMaxModels; ++i)
-      if (i < M) rec[i] = sh[g2][tl][i];
-    if (pick(rec, s).x == -INFINITY) continue;  // group saw no tile
-    absorb(st, M, s, ct, rec);
-  }
 
   const int64_t y = a.labels[t];
   const bool valid = y != a.ignore_index && y >= 0 && y < a.V;
   const int64_t T = a.T;
   float* lse1 = a.stats;
-  float* lset = a.stats + (int64_t)M * T;
-  float* ce_row = a.stats + 2 * (int64_t)M * T;
-  float* kl_row = a.stats + 3 * (int64_t)M * T;
-  float* h_row = a.stats + 4 * (int64_t)M * T;
-  const float m_s = pick(st.m, s), st_s = pick(st.st, s), xr_s = pick(st.xr, s);
-  const float lset_s = m_s * inv_tau + logf(st_s);
-  const float den = a.tau * st_s;
+  float* lset = a.stats + (int64_t)MM * T;
+  float* ce_row = a.stats + 2 * (int64_t)MM * T;
+  float* kl_row = a.stats + 3 * (int64_t)MM * T;
+  float* h_row = a.stats + 4 * (int64_t)MM * T;
+  const float lset_s = st.m[0] * inv_tau + logf(st.st[0]);
+  const float den = a.tau * st.st[0];
+  const float xr_s = st.xr[0];
 #pragma unroll
-  for (int i = 0; i < kMaxModels; ++i) {
-    if (i >= M) continue;
-    const float l1 = st.m[i] + logf(st.s1[i]);
-    const float lt = st.m[i] * inv_tau + logf(st.st[i]);
+  for (int k = 0; k < MM; ++k) {
+    const int64_t i = a.order[k];
+    const float l1 = st.m[k] + logf(st.s1[k]);
+    const float lt = st.m[k] * inv_tau + logf(st.st[k]);
     lse1[i * T + t] = l1;
     lset[i * T + t] = lt;
     ce_row[i * T + t] = valid ? l1 - a.lab[i * T + t] : 0.f;
-    kl_row[i * T + t] = (valid && i != s) ? (xr_s - st.xr[i]) / den - lset_s + lt : 0.f;
+    kl_row[i * T + t] = (valid && k != 0) ? (xr_s - st.xr[k]) / den - lset_s + lt : 0.f;
   }
   h_row[t] = valid ? lset_s - xr_s / den : 0.f;
 }
@@ -238,10 +231,26 @@ hipError_t launch_label_logits(const RowArgs& a, bool f32, hipStream_t stream) {
   return hipGetLastError();
 }
 
-hipError_t launch_finalize_rows(const RowArgs& a, hipStream_t stream) {
+template <int MM>
+hipError_t launch_finalize_rows_m(const RowArgs& a, hipStream_t stream) {
   dim3 grid((unsigned)((a.T + kRowTok - 1) / kRowTok));
-  hipLaunchKernelGGL(finalize_rows_kernel, grid, dim3(kThreads), 0, stream, a);
+  hipLaunchKernelGGL(finalize_rows_kernel<MM>, grid, dim3(kThreads), 0, stream, a);
   return hipGetLastError();
+}
+
+hipError_t launch_finalize_rows(const RowArgs& a, hipStream_t stream) {
+  static_assert(kMaxModels == 8, "one instantiation per model count");
+  switch (a.M) {
+    case 1: return launch_finalize_rows_m<1>(a, stream);
+    case 2: return launch_finalize_rows_m<2>(a, stream);
+    case 3: return launch_finalize_rows_m<3>(a, stream);
+    case 4: return launch_finalize_rows_m<4>(a, stream);
+    case 5: return launch_finalize_rows_m<5>(a, stream);
+    case 6: return launch_finalize_rows_m<6>(a, stream);
+    case 7: return launch_finalize_rows_m<7>(a, stream);
+    case 8: return launch_finalize_rows_m<8>(a, stream);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_reduce_losses(const RowArgs& a, hipStream_t stream) {
