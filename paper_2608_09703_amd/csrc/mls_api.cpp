@@ -213,7 +213,8 @@ void make_plan(const mls_problem* p, Plan& pl) {
     pl.n_tt_diag = (int)((p->T + diag_tile_cols(pl.wide, pl.M) - 1) / diag_tile_cols(pl.wide, pl.M));
     off = 0;
     pl.off_dpart = off;
-    off = align256(off + (size_t)pl.n_vt_diag * pl.T * diag_record_floats(pl.M) * sizeof(float));
+    off = align256(off + (size_t)pl.n_vt_diag * kDiagParts * pl.T * diag_record_floats(pl.M) *
+                             sizeof(float));
     pl.off_drow = off;
     off = align256(off + (size_t)pl.T * 2 * pl.M * pl.M * sizeof(float));
     pl.diag_bytes = off;

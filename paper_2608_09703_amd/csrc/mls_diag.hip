@@ -66,10 +66,8 @@ __global__ __launch_bounds__(Mma::NT, MINB) void diag_tile_kernel(DiagArgs a) {
   constexpr int FN = Mma::FN;
   using R = DiagRec<MM>;
   constexpr int REC = R::kFloats;
+  static_assert(WGM == kDiagParts, "one record per wave row");
   __shared__ __attribute__((aligned(16))) char smem[Mma::kSmemBytes];
-  // the per-wave partials of the epilogue reuse the operand staging buffer
-  static_assert(sizeof(float) * WGM * BN * REC <= Mma::kSmemBytes, "epilogue partials overflow LDS");
-  auto red = reinterpret_cast<float (*)[BN][REC]>(smem);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -91,7 +89,8 @@ __global__ __launch_bounds__(Mma::NT, MINB) void diag_tile_kernel(DiagArgs a) {
     mma[j].run(static_cast<const char*>(a.W[j]), kb, vbase, a.V, static_cast<const char*>(a.h[j]),
                kb, tbase, a.T, kb, smem, tid);
   }
-  __syncthreads();  // every wave is done reading operands from smem
+  // record of this wave row: [vocabulary tile * WGM + wm][field][token]
+  float* const out0 = a.partials + ((int64_t)vt * WGM + wm) * REC * a.T;
 
 #pragma unroll
   for (int fn = 0; fn < FN; ++fn) {
@@ -148,8 +147,8 @@ __global__ __launch_bounds__(Mma::NT, MINB) void diag_tile_kernel(DiagArgs a) {
             if (j != i) S[i][j] = fmaf(p[i], l[i] - l[j], S[i][j]);
       }
 
-    // lanes l and l ^ 32 hold the same token column: merge, then the WGM waves
-    // of the column through LDS
+    // lanes l and l ^ 32 hold the same token column: merge, and the lower
+    // half writes the wave's record (consecutive lanes, consecutive tokens)
 #pragma unroll
     for (int i = 0; i < MM; ++i) {
       float os[MM];
@@ -160,54 +159,26 @@ __global__ __launch_bounds__(Mma::NT, MINB) void diag_tile_kernel(DiagArgs a) {
       const int oi = __shfl_xor(bidx[i], 32, 64);
       merge_part<MM>(best[i], bidx[i], Z[i], S[i], ob, oi, oz, os);
     }
-    if (hi == 0) {
-      const int c = Mma::col_of(wn, fn, lane);
+    const int64_t t = tbase + Mma::col_of(wn, fn, lane);
+    if (hi == 0 && t < a.T) {
+      float* out = out0 + t;
 #pragma unroll
       for (int i = 0; i < MM; ++i) {
 #pragma unroll
-        for (int j = 0; j < MM; ++j) red[wm][c][R::kS + i * MM + j] = S[i][j];
-        red[wm][c][R::kZ + i] = Z[i];
-        red[wm][c][R::kBest + i] = best[i];
-        red[wm][c][R::kIdx + i] = __int_as_float(bidx[i]);
+        for (int j = 0; j < MM; ++j) out[(int64_t)(R::kS + i * MM + j) * a.T] = S[i][j];
+        out[(int64_t)(R::kZ + i) * a.T] = Z[i];
+        out[(int64_t)(R::kBest + i) * a.T] = best[i];
+        out[(int64_t)(R::kIdx + i) * a.T] = __int_as_float(bidx[i]);
       }
     }
   }
-  __syncthreads();
-  // merge the WGM waves of a column and write the record, layout
-  // [vocabulary tile][field][token]: consecutive threads write consecutive
-  // tokens. One thread takes one (token, sub-model) pair.
-  for (int idx = tid; idx < BN * MM; idx += Mma::NT) {
-    const int c = idx % BN;
-    const int i = idx / BN;
-    const int64_t t = tbase + c;
-    if (t >= a.T) continue;
-    float b = red[0][c][R::kBest + i];
-    int bi = __float_as_int(red[0][c][R::kIdx + i]);
-    float z = red[0][c][R::kZ + i];
-    float s[MM];
-#pragma unroll
-    for (int j = 0; j < MM; ++j) s[j] = red[0][c][R::kS + i * MM + j];
-#pragma unroll
-    for (int w = 1; w < WGM; ++w) {
-      float os[MM];
-#pragma unroll
-      for (int j = 0; j < MM; ++j) os[j] = red[w][c][R::kS + i * MM + j];
-      merge_part<MM>(b, bi, z, s, red[w][c][R::kBest + i], __float_as_int(red[w][c][R::kIdx + i]),
-                     red[w][c][R::kZ + i], os);
-    }
-    float* out = a.partials + (int64_t)vt * REC * a.T + t;
-#pragma unroll
-    for (int j = 0; j < MM; ++j) out[(int64_t)(R::kS + i * MM + j) * a.T] = s[j];
-    out[(int64_t)(R::kZ + i) * a.T] = z;
-    out[(int64_t)(R::kBest + i) * a.T] = b;
-    out[(int64_t)(R::kIdx + i) * a.T] = __int_as_float(bi);
-  }
 }
 
-// Per token: merge the records of all vocabulary tiles, finish KL(p_i || p_j)
-// and the argmax, and write the per-token values the mean reduction reads. A
-// block takes kRowTok tokens; its kRowSlices thread rows each merge every
-// kRowSlices-th vocabulary tile, and the slices are merged in a fixed order.
+// Per token: merge the records of all vocabulary tiles (kDiagParts per tile),
+// finish KL(p_i || p_j) and the argmax, and write the per-token values the
+// mean reduction reads. A block takes kRowTok tokens; its kRowSlices thread
+// rows each merge every kRowSlices-th record, and the slices are merged in a
+// fixed order.
 constexpr int kRowTok = 32;
 constexpr int kRowSlices = 16;
 
@@ -230,8 +201,8 @@ __global__ __launch_bounds__(kRowTok * kRowSlices) void diag_rows_kernel(DiagArg
     for (int j = 0; j < MM; ++j) S[i][j] = 0.f;
   }
   if (t < a.T) {
-    for (int vt = g; vt < a.n_vt; vt += kRowSlices) {
-      const float* in = a.partials + (int64_t)vt * REC * a.T + t;
+    for (int q = g; q < a.n_vt * kDiagParts; q += kRowSlices) {
+      const float* in = a.partials + (int64_t)q * REC * a.T + t;
 #pragma unroll
       for (int i = 0; i < MM; ++i) {
         float os[MM];

@@ -17,6 +17,8 @@ constexpr int kFusedWideBM = 128;  // wide bf16 core (all widths multiples of 64
 // forward partial records per (vocabulary tile, token, sub-model): one per
 // wave row of the tile, each over its own half of the tile's rows
 constexpr int kFusedFwdParts = 2;
+// diagnostics records per (vocabulary tile, token), one per wave row likewise
+constexpr int kDiagParts = 2;
 constexpr int kFusedBN = 128;
 // Tile of the backward GEMMs.
 constexpr int kGemmBM = 128;
@@ -153,7 +155,7 @@ struct DiagArgs {
   int32_t n_tt;
   int32_t n_vt;
   int32_t group_v;        // tile order: vocabulary tiles per group
-  float* partials;        // [n_vt][M*M + 3M][T]
+  float* partials;        // [n_vt * kDiagParts][M*M + 3M][T]
   float* rowvals;         // [T][2*M*M]
   float* kl_pair;         // [M][M]
   float* agree;           // [M][M]
