@@ -130,10 +130,12 @@ typedef struct mls_problem {
  * Sizes of the two caller-allocated device buffers for problem p.
  *   workspace_bytes  scratch for one call of mls_distill_fwd, mls_distill_bwd
  *                    or mls_diagnostics (contents are not kept between calls).
- *                    It is the largest of the three needs: the backward's
- *                    per-chunk logit-gradient slab, or the diagnostics'
- *                    (M*M + 3M) floats per token and 128-row vocabulary tile
- *                    (the larger one at V = 262144, T = 32768).
+ *                    It is the largest of three needs: the forward's two
+ *                    16-byte partial records per sub-model, token and 128-row
+ *                    vocabulary tile; the backward's per-chunk logit-gradient
+ *                    slab (normally the largest); the
+ *                    diagnostics' two records of (M*M + 3M) floats per token
+ *                    and 128-row vocabulary tile.
  *   stats_bytes      per-row statistics the forward writes and the backward
  *                    reads. Layout (all little-endian, offsets in elements of
  *                    float32 from the start):

@@ -104,9 +104,10 @@ def test_wide_backward_operands_stay_below_4_gib():
     T, V = 1 << 22, 4096
     # explicit whole-vocabulary chunk: an uncapped slab would take T * V * 2 = 32 GiB
     ws_wide, _ = B.query_sizes(_fake_problem(M=1, dims=[64], T=T, V=V, vocab_chunk=V))
-    # the forward's partial records (64-bit indexed) are the larger need here
+    # the forward's and the diagnostics' records (64-bit indexed) are the larger needs here
     fwd = 2 * (V // 128) * T * 16 + T * 4
-    assert ws_wide <= max((1 << 32) - 1, fwd + 512)
+    diag = 2 * (V // 128) * T * 4 * 4 + T * 2 * 4
+    assert ws_wide <= max((1 << 32) - 1, fwd, diag) + 512
     # widths that are not multiples of 64 take the general kernels: no cap there
     ws_gen, _ = B.query_sizes(_fake_problem(M=1, dims=[72], T=T, V=V, vocab_chunk=V))
     assert ws_gen >= 2 * T * V * 2
