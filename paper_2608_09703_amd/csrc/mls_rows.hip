@@ -103,9 +103,9 @@ __global__ __launch_bounds__(kThreads) void finalize_rows_kernel(RowArgs a) {
     st.st[i] = 0.f;
     st.xr[i] = 0.f;
   }
-  const int64_t n_tt = (a.T + kFusedBN - 1) / kFusedBN;
-  const float4* part = a.partials + (t / kFusedBN) * a.n_rec * kFusedBN + t % kFusedBN;
   if (t < a.T) {
+    const int64_t n_tt = (a.T + kFusedBN - 1) / kFusedBN;
+    const float4* part = a.partials + (t / kFusedBN) * a.n_rec * kFusedBN + t % kFusedBN;
 #pragma unroll 4
     for (int j = grp; j < a.n_rec; j += kRowGrp) {
       float4 rec[MM];
