@@ -79,8 +79,14 @@ enum mls_flags {
 
 /* Device-side error bits written into the statistics buffer by the forward. */
 enum mls_device_flags {
-  MLS_DEVFLAG_LABEL_RANGE = 1  /* a label outside [0, V) that is not ignore_index;
+  MLS_DEVFLAG_LABEL_RANGE = 1, /* a label outside [0, V) that is not ignore_index;
                                   such tokens are treated as ignored */
+  MLS_DEVFLAG_NONFINITE = 2    /* some token's log-sum-exp (ignored tokens included)
+                                  or a valid token's cross-entropy, KL or teacher
+                                  entropy is NaN or infinite: a non-finite value in
+                                  h_i or W_i. Losses of valid tokens, or the head
+                                  gradients (an ignored token's h_i row still enters
+                                  grad_W = G^T h), are then not meaningful. */
 };
 
 /*
@@ -98,6 +104,11 @@ enum mls_device_flags {
  *                 mls_distill_bwd is given no coefficient vectors
  *   tau           distillation temperature, finite and > 0 (1 = eq. (2) as printed)
  *   in_dtype      an mls_dtype
+ *   grad_h_dtype  mls_dtype of the grad_h_i outputs of mls_distill_bwd: MLS_F32, or
+ *                 MLS_BF16 (rounded once from the fp32 sums; over several
+ *                 vocabulary chunks the partial sums are kept in fp32 in the
+ *                 workspace). Note that 0 is MLS_BF16: a zero-filled struct asks
+ *                 for bf16 gradients.
  *   flags         OR of mls_flags
  *   vocab_chunk   backward vocabulary chunk width, rounded up to a multiple of
  *                 256; 0 = chosen by the library: at least four balanced
@@ -122,6 +133,7 @@ typedef struct mls_problem {
   float alpha;
   float tau;
   int32_t in_dtype;
+  int32_t grad_h_dtype;
   uint32_t flags;
   int64_t vocab_chunk;
 } mls_problem;
@@ -162,9 +174,10 @@ mls_status mls_distill_fwd(const mls_problem* p, void* stats, float* ce, float* 
                            void* stream);
 
 /*
- * Backward pass: grad_h[i] (device float32 [T, d[i]]) and grad_W[i] (device
- * float32 [V, d[i]]) of J = sum_i g_ce[i] CE_i + g_kl[i] KL_i, with the
- * teacher distribution under stop_grad.
+ * Backward pass: grad_h[i] (device [T, d[i]], float32 or bfloat16 as
+ * p->grad_h_dtype says) and grad_W[i] (device float32 [V, d[i]]) of
+ * J = sum_i g_ce[i] CE_i + g_kl[i] KL_i, with the teacher distribution under
+ * stop_grad (paper section 2, eq. (2) and eq. (3)).
  *   stats        the buffer written by mls_distill_fwd on the same inputs
  *   g_ce, g_kl   device float32 [M] coefficient vectors (e.g. the upstream
  *                gradients of ce and kl), read on the device so no host
@@ -172,13 +185,14 @@ mls_status mls_distill_fwd(const mls_problem* p, void* stats, float* ce, float* 
  *                of MLS_MODE_PAPER with p->alpha and p->tau are used. One NULL
  *                and one non-NULL is an error.
  *   grad_h       host array of M device pointers; an entry may be NULL to skip
- *                that gradient. Overwritten unless MLS_ACCUMULATE_GRAD_H.
+ *                that gradient. Overwritten unless MLS_ACCUMULATE_GRAD_H (a bf16
+ *                grad_h is then read, added to in fp32 and rounded once).
  *   grad_W       host array of M device pointers; an entry may be NULL.
  *                Overwritten unless MLS_ACCUMULATE_GRAD_W.
  * Asynchronous on stream.
  */
 mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float* g_ce,
-                           const float* g_kl, float* const* grad_h, float* const* grad_W,
+                           const float* g_kl, void* const* grad_h, float* const* grad_W,
                            void* workspace, size_t workspace_bytes, void* stream);
 
 /*
@@ -341,6 +355,19 @@ mls_status mls_coeffs(int32_t M, int32_t teacher, float alpha, float tau, int32_
  * statistics buffer. Synchronises the stream. Either output may be NULL. */
 mls_status mls_read_stats_header(const mls_problem* p, const void* stats, void* stream,
                                  int32_t* n_valid, int32_t* device_flags);
+
+/*
+ * Device-side errors of the forward pass (paper section 2, eq. (2) and
+ * eq. (3) need finite logits and labels in [0, V)): *flags receives the OR of
+ * mls_device_flags the last mls_distill_fwd (or mls_distill_fwd_bwd) on this
+ * statistics buffer raised: MLS_DEVFLAG_LABEL_RANGE for a label outside
+ * [0, V) that is not ignore_index, MLS_DEVFLAG_NONFINITE for a NaN or
+ * infinite per-token statistic of a valid token. The flags live in the
+ * statistics buffer's header (the forward rewrites them on every call), so
+ * calls on different buffers do not interfere. Waits for the stream: call it
+ * after the forward, not inside a timed or captured region.
+ */
+mls_status mls_device_error(const mls_problem* p, const void* stats, void* stream, int32_t* flags);
 
 /*
  * Kernel timing, a tracing aid for benchmarks. While enabled (per calling

@@ -32,7 +32,8 @@ def _dtype_code(dt: torch.dtype) -> int:
 
 def make_problem(h: Sequence[torch.Tensor], W: Sequence[torch.Tensor], labels: torch.Tensor, *,
                  alpha: float = 0.0, tau: float = 1.0, teacher: int = -1,
-                 ignore_index: int = -100, flags: int = 0, vocab_chunk: int = 0) -> B.Problem:
+                 ignore_index: int = -100, flags: int = 0, vocab_chunk: int = 0,
+                 grad_h_dtype: torch.dtype = torch.float32) -> B.Problem:
     M = len(h)
     if M < 1 or len(W) != M:
         raise ValueError("need one head per sub-model")
@@ -54,7 +55,8 @@ def make_problem(h: Sequence[torch.Tensor], W: Sequence[torch.Tensor], labels: t
     return B.make_problem(M, T, V, [x.shape[1] for x in h], [x.data_ptr() for x in h],
                           [x.data_ptr() for x in W], labels.data_ptr(), dtype=_dtype_code(dt),
                           teacher=teacher, ignore_index=ignore_index, alpha=alpha, tau=tau,
-                          flags=flags, vocab_chunk=vocab_chunk)
+                          flags=flags, vocab_chunk=vocab_chunk,
+                          grad_h_dtype=_dtype_code(grad_h_dtype))
 
 
 def _stream(dev) -> int:
@@ -90,9 +92,13 @@ def forward(p: B.Problem, buf: Buffers, device) -> None:
 def backward(p: B.Problem, buf: Buffers, device, g_ce: Optional[torch.Tensor],
              g_kl: Optional[torch.Tensor], grad_h: Sequence[Optional[torch.Tensor]],
              grad_W: Sequence[Optional[torch.Tensor]]) -> None:
-    for g in list(grad_h) + list(grad_W):
+    gh_dt = torch.bfloat16 if p.grad_h_dtype == B.MLS_BF16 else torch.float32
+    for g in grad_h:
+        if g is not None and (g.dtype != gh_dt or not g.is_contiguous()):
+            raise ValueError(f"grad_h tensors are contiguous {gh_dt} tensors")
+    for g in grad_W:
         if g is not None and (g.dtype != torch.float32 or not g.is_contiguous()):
-            raise ValueError("gradients are contiguous float32 tensors")
+            raise ValueError("grad_W tensors are contiguous float32 tensors")
     gc = g_ce.data_ptr() if g_ce is not None else None
     gk = g_kl.data_ptr() if g_kl is not None else None
     B.distill_bwd(p, buf.stats.data_ptr(), gc, gk,
@@ -106,7 +112,8 @@ class _Distill(torch.autograd.Function):
     def forward(ctx, labels, opts, *hw):
         M = len(hw) // 2
         h, W = list(hw[:M]), list(hw[M:])
-        p = make_problem(h, W, labels, **opts)
+        # bf16 hidden states get bf16 gradients straight from the library
+        p = make_problem(h, W, labels, grad_h_dtype=h[0].dtype, **opts)
         dev = h[0].device
         buf = Buffers(p, dev)
         forward(p, buf, dev)
@@ -132,8 +139,9 @@ class _Distill(torch.autograd.Function):
         need = ctx.needs_input_grad[2:]
         gh: List[Optional[torch.Tensor]] = []
         gW: List[Optional[torch.Tensor]] = []
+        gh_dt = torch.bfloat16 if ctx.p.grad_h_dtype == B.MLS_BF16 else torch.float32
         for i in range(M):
-            gh.append(torch.empty(hw[i].shape, dtype=torch.float32, device=dev) if need[i] else None)
+            gh.append(torch.empty(hw[i].shape, dtype=gh_dt, device=dev) if need[i] else None)
             gW.append(torch.empty(hw[M + i].shape, dtype=torch.float32, device=dev)
                       if need[M + i] else None)
         backward(ctx.p, ctx.buf, dev, g_ce, g_kl, gh, gW)

@@ -37,6 +37,7 @@ MLS_ACCUMULATE_GRAD_W = 1
 MLS_ACCUMULATE_GRAD_H = 2
 
 MLS_DEVFLAG_LABEL_RANGE = 1
+MLS_DEVFLAG_NONFINITE = 2
 
 EXPORTED = (
     "mls_query_sizes",
@@ -51,6 +52,7 @@ EXPORTED = (
     "mls_spec_verify",
     "mls_coeffs",
     "mls_read_stats_header",
+    "mls_device_error",
     "mls_status_string",
     "mls_last_error",
     "mls_version",
@@ -85,6 +87,7 @@ class Problem(ctypes.Structure):
         ("alpha", ctypes.c_float),
         ("tau", ctypes.c_float),
         ("in_dtype", ctypes.c_int32),
+        ("grad_h_dtype", ctypes.c_int32),
         ("flags", ctypes.c_uint32),
         ("vocab_chunk", ctypes.c_int64),
     ]
@@ -146,6 +149,7 @@ def lib():
                                  ctypes.c_int32, fp, fp, fp]
         L.mls_read_stats_header.argtypes = [P, vp, vp, ctypes.POINTER(ctypes.c_int32),
                                             ctypes.POINTER(ctypes.c_int32)]
+        L.mls_device_error.argtypes = [P, vp, vp, ctypes.POINTER(ctypes.c_int32)]
         L.mls_status_string.argtypes = [ctypes.c_int]
         L.mls_status_string.restype = ctypes.c_char_p
         L.mls_last_error.argtypes = []
@@ -158,7 +162,8 @@ def lib():
         L.mls_profile_report.argtypes = [ctypes.POINTER(KernelTime), ctypes.c_int32,
                                          ctypes.POINTER(ctypes.c_int32)]
         for name in ("mls_query_sizes", "mls_distill_fwd", "mls_distill_bwd", "mls_coeffs",
-                     "mls_read_stats_header", "mls_profile_enable", "mls_profile_report"):
+                     "mls_read_stats_header", "mls_device_error", "mls_profile_enable",
+                     "mls_profile_report"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -174,7 +179,8 @@ def check(status: int, where: str):
 def make_problem(M: int, T: int, V: int, dims: Sequence[int], h_ptrs: Sequence[int],
                  W_ptrs: Sequence[int], labels_ptr: int, *, dtype: int = MLS_BF16,
                  teacher: int = -1, ignore_index: int = -100, alpha: float = 0.0,
-                 tau: float = 1.0, flags: int = 0, vocab_chunk: int = 0) -> Problem:
+                 tau: float = 1.0, flags: int = 0, vocab_chunk: int = 0,
+                 grad_h_dtype: int = MLS_F32) -> Problem:
     p = Problem()
     p.M = M
     p.teacher = teacher
@@ -189,6 +195,7 @@ def make_problem(M: int, T: int, V: int, dims: Sequence[int], h_ptrs: Sequence[i
     p.alpha = alpha
     p.tau = tau
     p.in_dtype = dtype
+    p.grad_h_dtype = grad_h_dtype
     p.flags = flags
     p.vocab_chunk = vocab_chunk
     return p
@@ -297,6 +304,13 @@ def read_stats_header(p: Problem, stats: int, stream: int):
     check(lib().mls_read_stats_header(ctypes.byref(p), stats, stream, ctypes.byref(n),
                                       ctypes.byref(f)), "mls_read_stats_header")
     return n.value, f.value
+
+
+def device_error(p: Problem, stats: int, stream: int) -> int:
+    """OR of the MLS_DEVFLAG_* bits the last forward on ``stats`` raised (waits for the stream)."""
+    f = ctypes.c_int32(0)
+    check(lib().mls_device_error(ctypes.byref(p), stats, stream, ctypes.byref(f)), "mls_device_error")
+    return f.value
 
 
 def profile_enable(on: bool = True):

@@ -105,8 +105,9 @@ struct Plan {
   bool wide_bwd = false;
   // forward workspace
   size_t off_partials = 0, off_lab = 0, fwd_bytes = 0;
-  // backward workspace
-  size_t off_slab = 0, off_slabT = 0, off_hT = 0, off_WT = 0, bwd_bytes = 0;
+  // backward workspace (off_ghp: fp32 partial sums of a bf16 grad_h over vocabulary chunks)
+  bool grad_h_bf16 = false;
+  size_t off_slab = 0, off_slabT = 0, off_hT = 0, off_WT = 0, off_ghp = 0, bwd_bytes = 0;
   // diagnostics workspace (vocabulary segments of the pairwise pass)
   int n_vt_diag = 0, n_tt_diag = 0;
   size_t off_dpart = 0, off_drow = 0, diag_bytes = 0;
@@ -125,6 +126,8 @@ mls_status validate(const mls_problem* p) {
   if (p->V < 2 || p->V > (1ll << 30)) return fail(MLS_INVALID_ARG, "V=%lld out of range", (long long)p->V);
   if (p->in_dtype != MLS_BF16 && p->in_dtype != MLS_F32)
     return fail(MLS_UNSUPPORTED, "in_dtype=%d unsupported", p->in_dtype);
+  if (p->grad_h_dtype != MLS_BF16 && p->grad_h_dtype != MLS_F32)
+    return fail(MLS_UNSUPPORTED, "grad_h_dtype=%d unsupported", p->grad_h_dtype);
   if (!(p->tau > 0.0f) || !isfinite(p->tau)) return fail(MLS_INVALID_ARG, "tau must be finite and > 0");
   if (!isfinite(p->alpha) || p->alpha < 0.0f || p->alpha > 1.0f)
     return fail(MLS_INVALID_ARG, "alpha must be in [0, 1]");
@@ -185,6 +188,7 @@ void make_plan(const mls_problem* p, Plan& pl) {
   }
   pl.Vc = std::max<int64_t>(256, std::min(vc, vmax));
   pl.n_chunks = (int)((p->V + pl.Vc - 1) / pl.Vc);
+  pl.grad_h_bf16 = p->grad_h_dtype == MLS_BF16;
 
   size_t off = 0;
   pl.off_partials = off;
@@ -204,6 +208,10 @@ void make_plan(const mls_problem* p, Plan& pl) {
     off = align256(off + (size_t)pl.sumd * pl.T_pad * pl.es);
     pl.off_WT = off;
     off = align256(off + (size_t)pl.sumd * pl.Vc * pl.es);
+  }
+  if (pl.grad_h_bf16 && pl.n_chunks > 1) {
+    pl.off_ghp = off;
+    off = align256(off + (size_t)pl.sumd * pl.T * sizeof(float));
   }
   pl.bwd_bytes = off;
 
@@ -416,7 +424,7 @@ mls_status mls_distill_fwd(const mls_problem* p, void* stats, float* ce, float* 
 }
 
 mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float* g_ce,
-                           const float* g_kl, float* const* grad_h, float* const* grad_W,
+                           const float* g_kl, void* const* grad_h, float* const* grad_W,
                            void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error.clear();
   mls_status st = validate(p);
@@ -428,7 +436,8 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
   if (!aligned(stats, 16) || !aligned(workspace, 16))
     return fail(MLS_INVALID_ARG, "misaligned stats / workspace");
   for (int i = 0; i < p->M; ++i) {
-    if ((grad_h[i] && !aligned(grad_h[i], 4)) || (grad_W[i] && !aligned(grad_W[i], 4)))
+    if ((grad_h[i] && !aligned(grad_h[i], p->grad_h_dtype == MLS_BF16 ? 2 : 4)) ||
+        (grad_W[i] && !aligned(grad_W[i], 4)))
       return fail(MLS_INVALID_ARG, "misaligned gradient pointer %d", i);
   }
   Plan pl;
@@ -556,7 +565,24 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
         g.ldb = pl.Vc;
         g.cols = p->d[i];
       }
-      g.C = grad_h[i];
+      // grad_h: fp32 output accumulated over the chunks; a bf16 output keeps the
+      // partial sums of the earlier chunks in fp32 and is stored once, by the last
+      const bool last = c == pl.n_chunks - 1;
+      const bool acc_flag = (p->flags & MLS_ACCUMULATE_GRAD_H) != 0;
+      float* ghp = pl.grad_h_bf16 && pl.n_chunks > 1
+                       ? reinterpret_cast<float*>(ws + pl.off_ghp) + doff[i] * pl.T
+                       : nullptr;
+      if (!pl.grad_h_bf16) {
+        g.C = static_cast<float*>(grad_h[i]);
+        g.accumulate = (c > 0 || acc_flag) ? 1 : 0;
+      } else if (!last) {
+        g.C = ghp;
+        g.accumulate = c > 0 ? 1 : 0;
+      } else {
+        g.Cb = static_cast<uint16_t*>(grad_h[i]);
+        g.Cpart = ghp;
+        g.accumulate = acc_flag ? 1 : 0;
+      }
       g.ldc = p->d[i];
       g.ldc_rows = pl.T;
       // the chunk's rows past vrows read as zero from the head: the last,
@@ -567,7 +593,6 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
       g.tiles_m = (int)((pl.T + tbm - 1) / tbm);
       g.tiles_n = (int)((p->d[i] + tbn - 1) / tbn);
       g.tile_begin = tiles;
-      g.accumulate = (c > 0 || (p->flags & MLS_ACCUMULATE_GRAD_H)) ? 1 : 0;
       g.group_m = 8;
       tiles += g.tiles_m * g.tiles_n;
     }
@@ -969,6 +994,14 @@ mls_status mls_read_stats_header(const mls_problem* p, const void* stats, void* 
   if (n_valid) *n_valid = hdr[0];
   if (device_flags) *device_flags = hdr[1];
   return MLS_OK;
+}
+
+mls_status mls_device_error(const mls_problem* p, const void* stats, void* stream, int32_t* flags) {
+  if (!flags) {
+    g_last_error.clear();
+    return fail(MLS_INVALID_ARG, "flags is NULL");
+  }
+  return mls_read_stats_header(p, stats, stream, nullptr, flags);
 }
 
 mls_status mls_profile_enable(int32_t enable) {

@@ -263,6 +263,8 @@ __global__ __launch_bounds__(Mma::NT, 1) void fused_bwd_kernel(FusedArgs a) {
               const float pt = TAU1 ? p1 : (ok ? fast_exp2(fmaf(l, ct, -lts)) : 0.f);
               g[rr] = fmaf(cg, p1 - oh, ck * (pt - q_t.get(fm, fn, r)));
             }
+            // a selection, not a product: an ignored row's logits may be NaN
+            g[rr] = rv[fn] ? g[rr] : 0.f;
           }
           const int row0 = Mma::row_of(wm, fm, rg * 4, lane);
           store4<E>(slab + t * a.Vc + vloc + row0, g[0], g[1], g[2], g[3]);
@@ -367,6 +369,8 @@ __global__ __launch_bounds__(Mma::NT, MINB) void fused_bwd_wide_kernel(FusedArgs
               const float pt = TAU1 ? p1 : (ok ? fast_exp2(fmaf(l, ct, -lts)) : 0.f);
               g[rr] = fmaf(cg, p1 - oh, ck * (pt - q_t.get(fm, fn, r)));
             }
+            // a selection, not a product: an ignored row's logits may be NaN
+            g[rr] = rv[fn] ? g[rr] : 0.f;
           }
           const int v0 = Mma::row_of(wm, fm, rg * 4, lane);  // multiple of 4
           uint2 w;

@@ -13,6 +13,18 @@ namespace mls {
 
 namespace {
 
+// One output element: fp32 C (overwritten or accumulated) or bf16 Cb (see GemmGroup).
+__device__ __forceinline__ void store_out(const GemmGroup& g, int64_t idx, float v) {
+  if (g.Cb) {
+    if (g.Cpart) v += g.Cpart[idx];
+    if (g.accumulate) v += __uint_as_float((uint32_t)g.Cb[idx] << 16);
+    g.Cb[idx] = to_storage<Bf16>(v);
+  } else {
+    float* c = g.C + idx;
+    *c = g.accumulate ? *c + v : v;
+  }
+}
+
 template <typename E>
 __global__ __launch_bounds__(kThreads, 2) void gemm_nt_kernel(GemmArgs a) {
   using Mma = TileMma<E, kGemmBM, kGemmBN, 2, 2>;
@@ -49,10 +61,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_nt_kernel(GemmArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int64_t m = m0 + Mma::row_of(wm, fm, r, lane);
-        if (m < g.rows && n < g.cols) {
-          float* c = g.C + m * g.ldc + n;
-          *c = g.accumulate ? *c + mma.acc[fm][fn][r] : mma.acc[fm][fn][r];
-        }
+        if (m < g.rows && n < g.cols) store_out(g, m * g.ldc + n, mma.acc[fm][fn][r]);
       }
     }
 }
@@ -89,10 +98,7 @@ __device__ __forceinline__ void wide_tile(const GemmGroup& g, int tm, int tn, in
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int64_t m = m0 + Mma::row_of(wm, fm, r, lane);
-        if (m < mext && n < next) {
-          float* c = g.C + m * g.ldc + n;
-          *c = g.accumulate ? *c + mma.acc[fm][fn][r] : mma.acc[fm][fn][r];
-        }
+        if (m < mext && n < next) store_out(g, m * g.ldc + n, mma.acc[fm][fn][r]);
       }
       __builtin_amdgcn_sched_barrier(0);  // one 32x32 block of stores at a time
     }

@@ -66,10 +66,15 @@ struct FusedArgs {
 };
 
 // One output matrix of a grouped NT GEMM: C[m][n] (+)= sum_k A[m][k] B[n][k].
+// With Cb set the result goes to the bf16 matrix Cb instead, as
+//   Cb[m][n] = bf16(sum + (Cpart ? Cpart[m][n] : 0) + (accumulate ? Cb[m][n] : 0))
+// (Cpart: fp32 partial sums of earlier vocabulary chunks, same layout).
 struct GemmGroup {
   const void* A;
   const void* B;
   float* C;
+  uint16_t* Cb;
+  const float* Cpart;
   int64_t lda;  // elements
   int64_t ldb;
   int64_t ldc;

@@ -170,7 +170,7 @@ __device__ __forceinline__ double wave_sum(double v) {
 constexpr int kRedThreads = 1024;
 
 __global__ __launch_bounds__(kRedThreads) void reduce_losses_kernel(RowArgs a) {
-  constexpr int kQ = 2 * kMaxModels + 3;  // ce[8], kl[8], h, count, flag
+  constexpr int kQ = 2 * kMaxModels + 4;  // ce[8], kl[8], h, count, flag, sum of every lse
   __shared__ double part[kRedThreads / 64][kQ];
   const int M = a.M;
   const int64_t T = a.T;
@@ -180,6 +180,7 @@ __global__ __launch_bounds__(kRedThreads) void reduce_losses_kernel(RowArgs a) {
   const float* ce_row = a.stats + 2 * (int64_t)M * T;
   const float* kl_row = a.stats + 3 * (int64_t)M * T;
   const float* h_row = a.stats + 4 * (int64_t)M * T;
+  const float* lse = a.stats;  // lse1[M][T] then lset[M][T]
   for (int64_t t = threadIdx.x; t < T; t += kRedThreads) {
     const int64_t y = a.labels[t];
     if (y != a.ignore_index) {
@@ -191,6 +192,7 @@ __global__ __launch_bounds__(kRedThreads) void reduce_losses_kernel(RowArgs a) {
       if (i >= M) continue;
       acc[i] += ce_row[i * T + t];
       acc[kMaxModels + i] += kl_row[i * T + t];
+      acc[2 * kMaxModels + 3] += (double)lse[i * T + t] + (double)lse[(M + i) * T + t];
     }
     acc[2 * kMaxModels] += h_row[t];
   }
@@ -215,8 +217,13 @@ __global__ __launch_bounds__(kRedThreads) void reduce_losses_kernel(RowArgs a) {
     a.kl[i] = i == a.teacher ? 0.f : (float)(tot[kMaxModels + i] * inv);
   }
   if (a.entropy) *a.entropy = (float)(tot[2 * kMaxModels] * inv);
+  // losses of ignored tokens are exact zeros; the log-sum-exp rows of every
+  // token (ignored ones too) are summed as well
+  bool finite = isfinite(tot[2 * kMaxModels]) && isfinite(tot[2 * kMaxModels + 3]);
+  for (int i = 0; i < M; ++i) finite = finite && isfinite(tot[i]) && isfinite(tot[kMaxModels + i]);
   a.header[0] = (int32_t)n;
-  a.header[1] = tot[2 * kMaxModels + 2] > 0 ? MLS_DEVFLAG_LABEL_RANGE : 0;
+  a.header[1] = (tot[2 * kMaxModels + 2] > 0 ? MLS_DEVFLAG_LABEL_RANGE : 0) |
+                (finite ? 0 : MLS_DEVFLAG_NONFINITE);
 }
 
 }  // namespace

@@ -11,7 +11,8 @@ from paper_2608_09703_amd import api as D
 LOSS_RTOL = 1e-3     # losses: relative 1e-3 ...
 LOSS_ATOL = 1e-5     # ... with an absolute floor for values near 0 (KL of equal models)
 ROW_ATOL = 5e-5      # per-row statistics: fp32 log-sum-exp of ~1e5 terms
-GRAD_RTOL = 2e-2     # gradients: relative Frobenius norm per tensor
+from tests.grad_checks import (GRAD_RTOL, assert_grad, assert_grad_rows,  # noqa: F401
+                                non_label_rows, rel_fro)
 
 
 def to_np(xs):
@@ -66,13 +67,3 @@ def assert_rows(gpu, ref, rows=None, what=""):
     np.testing.assert_allclose(g, ref["h_row"], rtol=LOSS_RTOL, atol=ROW_ATOL, err_msg=f"{what} H")
 
 
-def rel_fro(a, b):
-    nb = np.linalg.norm(b)
-    return np.linalg.norm(a - b) / (nb if nb > 0 else 1.0)
-
-
-def assert_grad(g, ref, what="", rtol=GRAD_RTOL):
-    assert np.all(np.isfinite(g)), f"{what}: non-finite gradient"
-    err = rel_fro(g, ref)
-    assert err <= rtol, f"{what}: relative Frobenius error {err:.3e} > {rtol}"
-    return err

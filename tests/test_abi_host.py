@@ -129,6 +129,8 @@ def test_wide_backward_operands_stay_below_4_gib():
     ("alpha", math.nan, B.MLS_INVALID_ARG),
     ("alpha", 1.5, B.MLS_INVALID_ARG),
     ("in_dtype", 7, B.MLS_UNSUPPORTED),
+    ("grad_h_dtype", 2, B.MLS_UNSUPPORTED),
+    ("grad_h_dtype", -1, B.MLS_UNSUPPORTED),
     ("vocab_chunk", -5, B.MLS_INVALID_ARG),
     ("labels", None, B.MLS_INVALID_ARG),
 ])
@@ -183,6 +185,42 @@ def test_backward_rejects_bad_arguments_before_device_work():
     with pytest.raises(B.MlsError) as e:
         B.distill_bwd(p, fake, None, None, grads, grads, fake + (1 << 20), 16, None)
     assert e.value.status == B.MLS_WORKSPACE_TOO_SMALL
+
+
+def test_bf16_grad_h_keeps_fp32_partial_sums_over_chunks():
+    """A bf16 grad_h over several vocabulary chunks needs fp32 partial sums of every
+    sub-model's grad_h in the workspace (T * sum(d) * 4 bytes); in one chunk it does not."""
+    M, T, dims = 3, 4096, [1024, 2048, 3072]
+    f32 = B.query_sizes(_fake_problem())[0]
+    b16 = B.query_sizes(_fake_problem(grad_h_dtype=B.MLS_BF16))[0]
+    assert b16 - f32 >= T * sum(dims) * 4
+    one = _fake_problem(vocab_chunk=50304)
+    one_b16 = _fake_problem(vocab_chunk=50304, grad_h_dtype=B.MLS_BF16)
+    assert B.query_sizes(one)[0] == B.query_sizes(one_b16)[0]
+
+
+def test_bf16_grad_h_alignment_checked_on_host():
+    p = _fake_problem(grad_h_dtype=B.MLS_BF16)
+    ws, st = B.query_sizes(p)
+    fake = 1 << 40
+    gW = [fake + (1 << 30) * (i + 1) for i in range(3)]
+    gh = [fake + (1 << 34) + (1 << 30) * i for i in range(3)]
+    gh[2] += 1  # odd address: not even 2-byte aligned
+    with pytest.raises(B.MlsError) as e:
+        B.distill_bwd(p, fake, None, None, gh, gW, fake + (1 << 20), ws, None)
+    assert e.value.status == B.MLS_INVALID_ARG
+
+
+def test_device_error_rejects_null_outputs_before_device_work():
+    p = _fake_problem()
+    f = ctypes.c_int32(0)
+    assert B.lib().mls_device_error(ctypes.byref(p), 1 << 40, None, None) == B.MLS_INVALID_ARG
+    assert B.lib().mls_device_error(ctypes.byref(p), None, None, ctypes.byref(f)) == B.MLS_INVALID_ARG
+    assert B.lib().mls_last_error() != b""
+    bad = _fake_problem()
+    bad.M = 0
+    assert B.lib().mls_device_error(ctypes.byref(bad), 1 << 40, None,
+                                    ctypes.byref(f)) == B.MLS_INVALID_ARG
 
 
 def test_chunk_width_is_rounded():

@@ -27,3 +27,19 @@ def test_a_second_rank_is_refused():
     r = _run(["--steps", "1"], env={"WORLD_SIZE": "2"})
     assert r.returncode == 2
     assert "error" in json.loads(r.stdout.strip().splitlines()[-1])
+
+
+def test_cpu_baseline_host_facts():
+    """Every CPU baseline records the oracle's threads, the host's CPU count and
+    model, and the BLAS library numpy calls."""
+    sys.path.insert(0, ROOT)
+    import bench
+    info = bench.host_info(3)
+    assert info["cores"] == 3
+    assert info["host_cpus"] == os.cpu_count()
+    assert isinstance(info["cpu_model"], str) and info["cpu_model"]
+    assert isinstance(info["blas"], str) and info["blas"]
+    st = bench.step_stats([3.0, 1.0, 2.0, 10.0])
+    assert st["median"] == 2.5 and st["n"] == 4 and st["max"] == 10.0
+    assert "36%" in bench.PAPER_CONTEXT["training_compute"]
+    assert "14%" in bench.PAPER_CONTEXT["speculative_decoding"]

@@ -46,3 +46,8 @@ def test_bench_line_contract(extra):
     cpu = out["cpu_baseline"]
     assert cpu["kind"] == "oracle" and cpu["value"] > 0 and cpu["cores"] >= 1
     assert cpu["unit"] == out["unit"] and cpu["sample"]
+    for k in ("host_cpus", "cpu_model", "blas"):
+        assert k in cpu, k
+    assert "paper_context" in out
+    if "ms_per_step_stats" in out:
+        assert out["ms_per_step"] == out["ms_per_step_stats"]["median"]

@@ -14,7 +14,8 @@ import torch
 
 import oracle
 from paper_2608_09703_amd import workloads as WL
-from tests.gpu_helpers import (assert_grad, assert_losses, assert_rows, rel_fro, run_gpu, to_np)
+from tests.gpu_helpers import (assert_grad, assert_grad_rows, assert_losses, assert_rows,
+                               non_label_rows, rel_fro, run_gpu, to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -64,14 +65,23 @@ def test_small_full_parity(case):
     assert_losses(gpu, ref, name)
     assert_rows(gpu, ref, what=name)
     gh, gW = oracle.backward(hn, Wn, yn, g_ce, g_kl, tau=wl.tau, teacher=teacher)
-    for i in range(wl.M):
-        e1 = assert_grad(gpu["grad_h"][i], gh[i], f"{name} grad_h[{i}]")
-        e2 = assert_grad(gpu["grad_W"][i], gW[i], f"{name} grad_W[{i}]")
+    check_head_grads(gpu, gh, gW, yn, wl.V, name)
+
+
+def check_head_grads(gpu, gh, gW, yn, V, name):
+    """Every row of grad_h and grad_W, the softmax-only rows of grad_W (no valid
+    token's label) on their own, the vocabulary tail, and exact zeros on ignored rows."""
+    soft = non_label_rows(V, yn)
+    for i in range(len(gh)):
+        e1 = assert_grad_rows(gpu["grad_h"][i], gh[i], f"{name} grad_h[{i}]")
+        e2 = assert_grad_rows(gpu["grad_W"][i], gW[i], f"{name} grad_W[{i}]", softmax_rows=soft)
         # vocabulary tail (rows past the last multiple of 256)
-        tail = (wl.V // 256) * 256
-        if tail < wl.V:
+        tail = (V // 256) * 256
+        if tail < V:
             assert_grad(gpu["grad_W"][i][tail:], gW[i][tail:], f"{name} grad_W[{i}] tail")
-        print(f"  sub-model {i}: grad_h err {e1:.2e}, grad_W err {e2:.2e}", flush=True)
+        print(f"  sub-model {i}: grad_h err {e1['tensor']:.2e} (worst row {e1['worst_row']:.2e}), "
+              f"grad_W err {e2['tensor']:.2e} (worst row {e2['worst_row']:.2e}, softmax-only rows "
+              f"{e2.get('softmax_rows', 0.0):.2e})", flush=True)
         ignored = yn == oracle.IGNORE_INDEX
         assert np.all(gpu["grad_h"][i][ignored] == 0)
 
@@ -88,6 +98,10 @@ def test_all_labels_ignored():
 
 
 def test_identical_student_has_zero_kl():
+    """A student equal to the teacher has KL = 0 and no KL gradient. The recompute
+    backward holds the teacher's q as bf16 in registers, so its logit gradient there
+    is at most 2^-9 q / (tau N) per entry; the gradient is bounded by that, entry by
+    entry, through |W|. It is also far below a genuine student's gradient."""
     wl = WL.custom(3, 256, (128, 64, 128), 3000, tau=1.7, w_std=0.1, seed=12)
     h, W, y = WL.make_inputs(wl, device=DEV)
     h[0] = h[2].clone()
@@ -96,7 +110,13 @@ def test_identical_student_has_zero_kl():
     assert abs(gpu["kl"][0]) < 1e-5
     assert gpu["kl"][1] > 1e-2
     assert np.abs(gpu["kl_row"][0]).max() < 1e-5
-    assert np.abs(gpu["grad_h"][0]).max() <= 1e-7 * max(1.0, np.abs(gpu["grad_h"][1]).max())
+    hn, Wn, yn = to_np(h), to_np(W), y.cpu().numpy()
+    q = np.exp(oracle.teacher_logq(hn, Wn, tau=wl.tau))
+    N = oracle.n_valid(yn)
+    bound = 2.0 ** -9 / (wl.tau * N) * (q @ np.abs(Wn[0].astype(np.float64)))
+    g0 = np.abs(gpu["grad_h"][0].astype(np.float64))
+    assert np.all(g0 <= 1.01 * bound + 1e-12), float((g0 - bound).max())
+    assert g0.max() <= 1e-2 * np.abs(gpu["grad_h"][1]).max()
 
 
 def test_uniform_logits_give_ln_v():
@@ -139,9 +159,7 @@ def test_default_coefficients_follow_alpha():
     gpu = run_gpu(h, W, y, tau=2.0, alpha=0.25)
     g_ce, g_kl = oracle.coeffs(3, -1, alpha=0.25, tau=2.0)
     gh, gW = oracle.backward(hn, Wn, yn, g_ce, g_kl, tau=2.0)
-    for i in range(3):
-        assert_grad(gpu["grad_h"][i], gh[i], f"grad_h[{i}]")
-        assert_grad(gpu["grad_W"][i], gW[i], f"grad_W[{i}]")
+    check_head_grads(gpu, gh, gW, yn, wl.V, "default coefficients")
 
 
 def test_autograd_front_end():
@@ -162,9 +180,10 @@ def test_autograd_front_end():
     np.testing.assert_allclose(ce.detach().cpu().numpy(), ref["ce"], rtol=1e-3)
     np.testing.assert_allclose(kl.detach().cpu().numpy()[:2], ref["kl"][:2], rtol=1e-3)
     gh, gW = oracle.backward(hn, Wn, yn, g_ce, g_kl, tau=1.5)
+    soft = non_label_rows(wl.V, yn)
     for i in range(3):
-        assert_grad(hs[i].grad.float().cpu().numpy(), gh[i], f"grad_h[{i}]")
-        assert_grad(Ws[i].grad.float().cpu().numpy(), gW[i], f"grad_W[{i}]")
+        assert_grad_rows(hs[i].grad.float().cpu().numpy(), gh[i], f"grad_h[{i}]")
+        assert_grad_rows(Ws[i].grad.float().cpu().numpy(), gW[i], f"grad_W[{i}]", softmax_rows=soft)
 
 
 # ---------------------------------------------------------------------------
@@ -195,7 +214,7 @@ def test_full_size_sampled_rows(name):
                                    rtol=1e-5)
     ghr = oracle.grad_h_rows(hn, Wn, yn, rows[:32], g_ce, g_kl, tau=wl.tau)
     for i in range(wl.M):
-        assert_grad(gpu["grad_h"][i][rows[:32]], ghr[i], f"{name} grad_h[{i}] rows")
+        assert_grad_rows(gpu["grad_h"][i][rows[:32]], ghr[i], f"{name} grad_h[{i}] rows")
         # every row of the logit gradient sums to zero: sum_v grad_W = 0
         colsum = gpu["grad_W"][i].astype(np.float64).sum(axis=0)
         scale = np.abs(gpu["grad_W"][i]).astype(np.float64).sum(axis=0).max()
@@ -205,23 +224,28 @@ def test_full_size_sampled_rows(name):
             assert np.all(gpu["grad_h"][i][ign] == 0)
 
 
-@pytest.mark.parametrize("name", ["c2_m3_v50k", "c3_m3_v128k_tau2"])
-def test_reduced_T_full_head_gradient(name):
-    """Same V, widths and distributions with T = 512: every grad_W element checked."""
-    wl = WL.WORKLOADS[name].replace(T=512)
-    print(f"[parity-reducedT] {name} T={wl.T} V={wl.V}", flush=True)
-    h, W, y, hn, Wn, yn = _inputs(wl)
+REDUCED_T = [("c2_m3_v50k", 512), ("c3_m3_v128k_tau2", 512), ("c4_m4_v128k_peaky", 256),
+             ("c5_m3_v262k_long", 256), ("paper3b_heads", 512)]
+
+
+@pytest.mark.parametrize("name,T", REDUCED_T, ids=[n for n, _ in REDUCED_T])
+def test_reduced_T_full_head_gradient(name, T):
+    """The workload's own V, widths, head scale, ignore fraction, alpha and tau with
+    fewer tokens: every row of grad_h and grad_W checked against the oracle."""
+    wl = WL.WORKLOADS[name].replace(T=T)
+    print(f"[parity-reducedT] {name} T={wl.T} V={wl.V} dims={wl.dims}", flush=True)
+    h, W, y = WL.make_inputs(wl, device=DEV)
+    hn = [x.double().cpu().numpy() for x in h]
+    Wn = [x.double().cpu().numpy() for x in W]
+    yn = y.cpu().numpy()
     g_ce, g_kl = _coeffs(wl.M, -1, wl.alpha, wl.tau)
     gpu = run_gpu(h, W, y, tau=wl.tau, g_ce=g_ce, g_kl=g_kl)
+    del h, W
     ref = oracle.forward(hn, Wn, yn, tau=wl.tau)
     assert_losses(gpu, ref, name)
+    assert_rows(gpu, ref, what=name)
     gh, gW = oracle.backward(hn, Wn, yn, g_ce, g_kl, tau=wl.tau)
-    for i in range(wl.M):
-        assert_grad(gpu["grad_h"][i], gh[i], f"{name} grad_h[{i}]")
-        assert_grad(gpu["grad_W"][i], gW[i], f"{name} grad_W[{i}]")
-        tail = (wl.V // 256) * 256
-        if tail < wl.V:
-            assert_grad(gpu["grad_W"][i][tail:], gW[i][tail:], f"{name} grad_W[{i}] tail")
+    check_head_grads(gpu, gh, gW, yn, wl.V, name)
 
 
 @pytest.mark.parametrize("name", ["c3_m3_v128k_tau2"])
@@ -284,3 +308,97 @@ def test_accumulate_flags_and_skipped_gradients(dtype, chunk):
         if gW[i] is not None:
             added = gW[i].cpu().numpy().astype(np.float64) - gW0[i].cpu().numpy()
             assert rel_fro(added, ref["grad_W"][i]) < 1e-5, f"grad_W {i}"
+
+
+@pytest.mark.parametrize("dims,dtype,chunk", [((64, 128, 192), "bf16", 512),
+                                              ((64, 128, 192), "bf16", 0),
+                                              ((72, 136, 200), "bf16", 256),
+                                              ((32, 36, 100), "f32", 256)],
+                         ids=["wide_chunks", "wide_default", "general_bf16", "general_f32"])
+def test_bf16_grad_h_is_the_rounded_fp32_gradient(dims, dtype, chunk):
+    """grad_h_dtype = bf16: the fp32 sums (kept in fp32 across vocabulary chunks) rounded
+    once, so the result equals the fp32 output rounded to bf16, bit for bit; with
+    MLS_ACCUMULATE_GRAD_H the old bf16 value is added in fp32 before the one rounding."""
+    from paper_2608_09703_amd import api as D
+    from paper_2608_09703_amd import binding as B
+    wl = WL.custom(3, 300, dims, 1500, dtype=dtype, tau=1.4, w_std=0.08, ignore_frac=0.1, seed=41)
+    print(f"[parity] bf16 grad_h dims={dims} {dtype} chunk={chunk}", flush=True)
+    h, W, y, hn, Wn, yn = _inputs(wl)
+    g_ce, g_kl = _coeffs(3, -1, 0.4, wl.tau)
+    gce = torch.tensor(g_ce, dtype=torch.float32, device=DEV)
+    gkl = torch.tensor(g_kl, dtype=torch.float32, device=DEV)
+    outs = {}
+    for gdt in (torch.float32, torch.bfloat16):
+        p = D.make_problem(h, W, y, tau=wl.tau, vocab_chunk=chunk, grad_h_dtype=gdt)
+        buf = D.Buffers(p, DEV)
+        D.forward(p, buf, DEV)
+        gh = [torch.full(x.shape, float("nan"), dtype=gdt, device=DEV) for x in h]
+        gW = [torch.empty(x.shape, dtype=torch.float32, device=DEV) for x in W]
+        D.backward(p, buf, DEV, gce, gkl, gh, gW)
+        outs[gdt] = (gh, gW)
+    torch.cuda.synchronize()
+    for i in range(3):
+        assert torch.equal(outs[torch.float32][0][i].to(torch.bfloat16), outs[torch.bfloat16][0][i])
+        assert torch.equal(outs[torch.float32][1][i], outs[torch.bfloat16][1][i])
+    gh_ref, _ = oracle.backward(hn, Wn, yn, g_ce, g_kl, tau=wl.tau)
+    for i in range(3):
+        assert_grad_rows(outs[torch.bfloat16][0][i].float().cpu().numpy(), gh_ref[i],
+                         f"bf16 grad_h[{i}]")
+    # accumulate into a bf16 gradient
+    p = D.make_problem(h, W, y, tau=wl.tau, vocab_chunk=chunk, grad_h_dtype=torch.bfloat16,
+                       flags=B.MLS_ACCUMULATE_GRAD_H)
+    buf = D.Buffers(p, DEV)
+    D.forward(p, buf, DEV)
+    g = torch.Generator(device=DEV).manual_seed(3)
+    gh0 = [(torch.randn(x.shape, generator=g, device=DEV) * float(r.float().std())).to(torch.bfloat16)
+           for x, r in zip(h, outs[torch.float32][0])]
+    gh = [x.clone() for x in gh0]
+    D.backward(p, buf, DEV, gce, gkl, gh, [None, None, None])
+    torch.cuda.synchronize()
+    for i in range(3):
+        want = (gh0[i].double() + outs[torch.float32][0][i].double())
+        got = gh[i].double()
+        # one rounding of a sum formed in fp32: within a bf16 half-ulp plus fp32 error
+        assert torch.all((got - want).abs() <= 2.0 ** -8 * want.abs() + 1e-30), i
+
+
+def test_nonfinite_input_flag():
+    """A NaN in a valid token's hidden state raises MLS_DEVFLAG_NONFINITE (and not the
+    label flag); one in an ignored token's hidden state raises it too (that row still
+    enters grad_W = G^T h) while the losses stay finite and equal the oracle's with the
+    row zeroed; finite inputs raise nothing."""
+    from paper_2608_09703_amd import api as D
+    from paper_2608_09703_amd import binding as B
+    wl = WL.custom(2, 200, (64, 128), 900, w_std=0.1, ignore_frac=0.2, seed=43)
+    h, W, y = WL.make_inputs(wl, device=DEV)
+    yn = y.cpu().numpy()
+    valid_t = int(np.flatnonzero(yn != -100)[3])
+    ign_t = int(np.flatnonzero(yn == -100)[0])
+
+    def flags_of(hh):
+        p = D.make_problem(hh, W, y)
+        buf = D.Buffers(p, DEV)
+        D.forward(p, buf, DEV)
+        f = B.device_error(p, buf.stats.data_ptr(), torch.cuda.current_stream(DEV).cuda_stream)
+        return f, buf
+
+    f, _ = flags_of(h)
+    assert f == 0
+    hv = [x.clone() for x in h]
+    hv[0][valid_t, 5] = float("nan")
+    f, buf = flags_of(hv)
+    assert f == B.MLS_DEVFLAG_NONFINITE
+    assert not np.isfinite(buf.ce.cpu().numpy()[0])
+    hi = [x.clone() for x in h]
+    hi[1][ign_t, :] = float("inf")
+    f, buf = flags_of(hi)
+    assert f == B.MLS_DEVFLAG_NONFINITE
+    hz = [x.clone() for x in h]
+    hz[1][ign_t, :] = 0
+    ref = oracle.forward(to_np(hz), to_np(W), yn)
+    np.testing.assert_allclose(buf.ce.cpu().numpy(), ref["ce"], rtol=1e-3, atol=1e-5)
+    np.testing.assert_allclose(buf.kl.cpu().numpy(), ref["kl"], rtol=1e-3, atol=1e-5)
+    # the ignored row's gradient is an exact zero even though its logits are not finite
+    gpu = run_gpu(hi, W, y, g_ce=[1.0, 1.0], g_kl=[0.5, 0.0])
+    assert np.all(gpu["grad_h"][1][ign_t] == 0)
+    assert np.all(np.isfinite(gpu["grad_h"][0])) and np.all(np.isfinite(gpu["grad_W"][0]))
