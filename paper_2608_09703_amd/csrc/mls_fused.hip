@@ -34,8 +34,10 @@ using GenMmaF32 = TileMma<F32, kFusedBM, kFusedBN, 2, 2>;
 using WideFused = WideMma<kFusedWideBM, kFusedBN, 2, 2, 2>;  // 2 blocks per CU
 
 // Per-lane copy of the teacher's tile values (its softmax weights), laid out
-// like the accumulators. The bf16 paths keep them as packed bf16 pairs
-// (half the registers; 2^-9 relative rounding), the fp32 path in fp32.
+// like the accumulators. The bf16 paths keep them as packed fp16 pairs (half
+// the registers; probabilities lie in [0, 1], where fp16 rounds to 2^-11
+// relative and flushes below 2^-24, an absolute error under 3e-8), the fp32
+// path in fp32.
 template <int FM, int FN, bool PACK>
 struct TeacherTile;
 
@@ -50,7 +52,7 @@ template <int FM, int FN>
 struct TeacherTile<FM, FN, true> {
   uint32_t v[FM][FN][8];
   __device__ __forceinline__ void set(int fm, int fn, int r, float x) {
-    const uint32_t b = to_storage<Bf16>(x);
+    const uint32_t b = __builtin_bit_cast(uint16_t, (_Float16)x);
     if (r & 1)
       v[fm][fn][r >> 1] = (v[fm][fn][r >> 1] & 0xffffu) | (b << 16);
     else
@@ -58,7 +60,7 @@ struct TeacherTile<FM, FN, true> {
   }
   __device__ __forceinline__ float get(int fm, int fn, int r) const {
     const uint32_t w = v[fm][fn][r >> 1];
-    return __uint_as_float((r & 1) ? (w & 0xffff0000u) : (w << 16));
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)((r & 1) ? (w >> 16) : (w & 0xffffu)));
   }
 };
 

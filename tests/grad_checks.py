@@ -15,7 +15,12 @@ from __future__ import annotations
 import numpy as np
 
 GRAD_RTOL = 2e-2      # relative Frobenius bound per tensor, per row, and on the softmax-only rows
-ROW_FLOOR = 1e-3      # absolute floor of the per-row bound, as a fraction of the median row norm
+# Absolute floor of the per-row bound, as a fraction of the median row norm. It
+# matters only for rows whose logit gradient nearly cancels (e.g. with two
+# vocabulary entries, p - (1 - alpha) onehot - alpha q can be far below its
+# terms): there the rounding of the terms (the slab's bf16, the teacher's q)
+# is absolute, a few 1e-4 of a typical row, not relative to the small result.
+ROW_FLOOR = 5e-3
 
 
 def rel_fro(a, b):
