@@ -341,6 +341,27 @@ mls_status mls_spec_verify(const mls_sampling* s, int64_t batch, int64_t gamma,
                            size_t workspace_bytes, void* stream);
 
 /*
+ * mls_spec_verify without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops). Same arguments,
+ * semantics and kernels as mls_spec_verify; the per-row distribution records
+ * (MLS_ROW_PARAMS_BYTES each, batch * (2 gamma + 1) of them) live in a static
+ * device array of MLS_SPEC_VERIFY_STATIC_BYTES that the library keeps on each
+ * device it runs on until the process ends. Problems needing more than that
+ * (mls_spec_verify_workspace reports the need) are rejected with
+ * MLS_INVALID_ARG before any device work. The call itself allocates nothing
+ * (its first call on a device looks up that device's copy of the array). All
+ * calls on one device share the array: calls that may overlap on one device
+ * (different streams, or different host threads, without ordering between
+ * them) race and must not be issued; calls ordered on one stream are safe.
+ */
+#define MLS_SPEC_VERIFY_STATIC_BYTES (2u << 20)
+mls_status mls_spec_verify_noalloc(const mls_sampling* s, int64_t batch, int64_t gamma,
+                                   const float* draft_logits, const float* target_logits,
+                                   const int32_t* draft_tokens, const float* u_accept,
+                                   const float* u_sample, const void* draft_params,
+                                   int32_t* n_accepted, int32_t* next_token, void* stream);
+
+/*
  * Host helper: loss coefficients of the objective (host arrays of length M).
  *   mode MLS_MODE_PAPER (eq. (3) summed over sub-models):
  *     student g_ce = w (1 - alpha), g_kl = w alpha tau^2; teacher g_ce = w, g_kl = 0

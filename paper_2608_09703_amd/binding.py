@@ -50,6 +50,7 @@ EXPORTED = (
     "mls_sample",
     "mls_spec_verify_workspace",
     "mls_spec_verify",
+    "mls_spec_verify_noalloc",
     "mls_coeffs",
     "mls_read_stats_header",
     "mls_device_error",
@@ -145,6 +146,8 @@ def lib():
                                                 ctypes.POINTER(ctypes.c_size_t)]
         L.mls_spec_verify.argtypes = [S, ctypes.c_int64, ctypes.c_int64, vp, vp, vp, vp, vp, vp, vp,
                                       vp, vp, ctypes.c_size_t, vp]
+        L.mls_spec_verify_noalloc.argtypes = [S, ctypes.c_int64, ctypes.c_int64, vp, vp, vp, vp,
+                                              vp, vp, vp, vp, vp]
         L.mls_coeffs.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_float, ctypes.c_float,
                                  ctypes.c_int32, fp, fp, fp]
         L.mls_read_stats_header.argtypes = [P, vp, vp, ctypes.POINTER(ctypes.c_int32),
@@ -279,6 +282,20 @@ def spec_verify(s: Sampling, batch: int, gamma: int, draft_logits: Optional[int]
     check(lib().mls_spec_verify(ctypes.byref(s), batch, gamma, draft_logits, target_logits,
                                 draft_tokens, u_accept, u_sample, draft_params, n_accepted,
                                 next_token, ws, ws_bytes, stream), "mls_spec_verify")
+
+
+SPEC_VERIFY_STATIC_BYTES = 2 << 20  # MLS_SPEC_VERIFY_STATIC_BYTES
+
+
+def spec_verify_noalloc(s: Sampling, batch: int, gamma: int, draft_logits: Optional[int],
+                        target_logits: int, draft_tokens: Optional[int], u_accept: Optional[int],
+                        u_sample: Optional[int], n_accepted: int, next_token: int, stream: int,
+                        draft_params: Optional[int] = None):
+    """mls_spec_verify with the library's static per-device scratch (no workspace)."""
+    check(lib().mls_spec_verify_noalloc(ctypes.byref(s), batch, gamma, draft_logits, target_logits,
+                                        draft_tokens, u_accept, u_sample, draft_params,
+                                        n_accepted, next_token, stream),
+          "mls_spec_verify_noalloc")
 
 
 def coeffs(M: int, teacher: int = -1, alpha: float = 0.0, tau: float = 1.0,

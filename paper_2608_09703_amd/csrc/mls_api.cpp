@@ -303,6 +303,12 @@ void host_coeffs(int M, int s, float alpha, float tau, int mode, const float* w,
 
 }  // namespace
 
+namespace mls {
+mls_status set_error(mls_status s, const char* what, const char* detail) {
+  return fail(s, detail && detail[0] ? "%s: %s" : "%s%s", what, detail ? detail : "");
+}
+}  // namespace mls
+
 extern "C" {
 
 const char* mls_version(void) { return "mls 0.1.0 (gfx950)"; }

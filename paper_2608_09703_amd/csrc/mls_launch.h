@@ -241,6 +241,9 @@ struct VerifyArgs {
   int32_t* next_token;         // [batch]
 };
 
+// Sets the calling thread's mls_last_error text to "what: detail" and returns s.
+mls_status set_error(mls_status s, const char* what, const char* detail);
+
 // Launchers (each enqueues on `stream` and returns the launch status).
 int fused_tile_rows(bool wide);
 hipError_t launch_fused_fwd(const FusedArgs& a, bool f32, hipStream_t stream);
