@@ -144,6 +144,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample rows (0 = auto)")
     ap.add_argument("--vocab-chunk", type=int, default=0)
+    ap.add_argument("--path", choices=("fwd_bwd", "recompute", "separate"), default="fwd_bwd",
+                    help="fwd_bwd: mls_distill_fwd_bwd with its default plan (stored logits per "
+                         "token chunk); recompute: the same call with MLS_FWD_BWD_RECOMPUTE; "
+                         "separate: mls_distill_fwd then mls_distill_bwd")
     ap.add_argument("--diagnostics", action="store_true",
                     help="time the pairwise diagnostics pass instead of fwd+bwd")
     ap.add_argument("--junction", action="store_true",
@@ -574,8 +578,13 @@ def main():
     log(f"workload {name}: M={wl.M} T={wl.T} dims={wl.dims} V={wl.V} {wl.dtype} "
         f"alpha={wl.alpha} tau={wl.tau}")
     h, W, y = WL.make_inputs(wl, device=dev)
-    p = D.make_problem(h, W, y, tau=wl.tau, alpha=wl.alpha, vocab_chunk=args.vocab_chunk)
+    flags = B.MLS_FWD_BWD_RECOMPUTE if args.path == "recompute" else 0
+    p = D.make_problem(h, W, y, tau=wl.tau, alpha=wl.alpha, vocab_chunk=args.vocab_chunk, flags=flags)
     buf = D.Buffers(p, dev)
+    if args.path != "separate" and not args.diagnostics:
+        fb_bytes = B.query_fwd_bwd_workspace(p)
+        if fb_bytes > buf.workspace.numel():
+            buf.workspace = torch.empty(fb_bytes, dtype=torch.uint8, device=dev)
     g_ce, g_kl = D.coefficients(wl.M, alpha=wl.alpha, tau=wl.tau)
     gce = torch.tensor(g_ce, dtype=torch.float32, device=dev)
     gkl = torch.tensor(g_kl, dtype=torch.float32, device=dev)
@@ -594,9 +603,14 @@ def main():
         if args.diagnostics:
             B.diagnostics(p, kl_pair.data_ptr(), agree.data_ptr(), None, ws_ptr, ws_n, sh)
             return
-        B.distill_fwd(p, st_ptr, buf.ce.data_ptr(), buf.kl.data_ptr(), buf.entropy.data_ptr(),
-                      ws_ptr, ws_n, sh)
-        B.distill_bwd(p, st_ptr, gce.data_ptr(), gkl.data_ptr(), gh_p, gW_p, ws_ptr, ws_n, sh)
+        if args.path == "separate":
+            B.distill_fwd(p, st_ptr, buf.ce.data_ptr(), buf.kl.data_ptr(), buf.entropy.data_ptr(),
+                          ws_ptr, ws_n, sh)
+            B.distill_bwd(p, st_ptr, gce.data_ptr(), gkl.data_ptr(), gh_p, gW_p, ws_ptr, ws_n, sh)
+        else:
+            B.distill_fwd_bwd(p, st_ptr, buf.ce.data_ptr(), buf.kl.data_ptr(),
+                              buf.entropy.data_ptr(), gce.data_ptr(), gkl.data_ptr(), gh_p, gW_p,
+                              ws_ptr, ws_n, sh)
 
     log(f"workspace {ws_n / 2**20:.0f} MiB, stats {buf.stats.numel() / 2**20:.1f} MiB")
     for k in range(args.warmup):
@@ -689,11 +703,12 @@ def main():
         "data": "synthetic (seeded Gaussian hidden states and heads, uniform labels)",
         "config": {"workload": name, "M": wl.M, "T": wl.T, "batch": wl.batch, "seq": wl.seq,
                    "widths": list(wl.dims), "V": wl.V, "alpha": wl.alpha, "tau": wl.tau,
-                   "ignore_frac": wl.ignore_frac, "parallelism": "single GPU"},
+                   "ignore_frac": wl.ignore_frac, "parallelism": "single GPU",
+                   "path": None if args.diagnostics else args.path},
         "pct_of_bf16_peak": pct if wl.dtype == "bf16" else None,
         "algorithmic_tflop_per_step": flops_step / 1e12,
-        # forward + backward execute the logits product once more (recompute): 8 T V sum(d)
-        "executed_tflop_per_step": flops_step * (1.0 if args.diagnostics else 4.0 / 3.0) / 1e12,
+        # a recomputing backward executes the logits product once more: 8 T V sum(d)
+        "executed_tflop_per_step": flops_step * (4.0 / 3.0 if "fused_bwd" in kernels else 1.0) / 1e12,
         "device": device,
         "roofline": roofline,
         "kernels": kernels,

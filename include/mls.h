@@ -74,7 +74,9 @@ enum mls_mode {
 
 enum mls_flags {
   MLS_ACCUMULATE_GRAD_W = 1u, /* grad_W_i += instead of = */
-  MLS_ACCUMULATE_GRAD_H = 2u  /* grad_h_i += instead of = */
+  MLS_ACCUMULATE_GRAD_H = 2u, /* grad_h_i += instead of = */
+  MLS_FWD_BWD_RECOMPUTE = 4u  /* mls_distill_fwd_bwd: recompute the logits in the backward
+                                 instead of storing them per token chunk */
 };
 
 /* Device-side error bits written into the statistics buffer by the forward. */
@@ -194,6 +196,36 @@ mls_status mls_distill_fwd(const mls_problem* p, void* stats, float* ce, float* 
 mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float* g_ce,
                            const float* g_kl, void* const* grad_h, float* const* grad_W,
                            void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Forward and backward in one call, for a caller that knows the objective's
+ * coefficients before the forward (a training step: J = sum_i g_ce[i] CE_i +
+ * g_kl[i] KL_i with eq. (3)'s coefficients, paper section 2, "Integrated
+ * Distillation", eq. (2) and eq. (3)). Same outputs as mls_distill_fwd followed by
+ * mls_distill_bwd with the same arguments (stats, losses, entropy, grad_h,
+ * grad_W, flags and grad_h_dtype as described there; g_ce / g_kl NULL means
+ * eq. (3) with p->alpha and p->tau).
+ *
+ * The logits are not recomputed: the tokens are taken in at least two chunks;
+ * for each, the forward stores every sub-model's logits of the chunk in the
+ * workspace (fp16 of each logit's distance to a local maximum over 64
+ * vocabulary entries, so the entries near the maximum, which carry the
+ * softmax's mass, are the most exact), the log-sum-exp rows are merged, the
+ * logit gradient is formed in place (bf16) and the two head products run on it
+ * (grad_h of the chunk's tokens complete, grad_W accumulated over the chunks).
+ * No [T, V] array exists at any time: a chunk holds at most
+ * ceil(T / 2) tokens, fewer when one sub-model's logits of a chunk would reach
+ * 4 GiB or all of them 16 GiB. Problems of one 128-token tile, widths that are
+ * not multiples of 64, fp32 inputs, heads [V, d_i] of 4 GiB or more, or
+ * MLS_FWD_BWD_RECOMPUTE in p->flags run the forward and then the recomputing
+ * backward instead. workspace_bytes: at least what mls_query_fwd_bwd_workspace
+ * reports. Asynchronous on stream.
+ */
+mls_status mls_query_fwd_bwd_workspace(const mls_problem* p, size_t* workspace_bytes);
+mls_status mls_distill_fwd_bwd(const mls_problem* p, void* stats, float* ce, float* kl,
+                               float* entropy, const float* g_ce, const float* g_kl,
+                               void* const* grad_h, float* const* grad_W, void* workspace,
+                               size_t workspace_bytes, void* stream);
 
 /*
  * Cross-model diagnostics (paper section 3, "Training Dynamics and Model

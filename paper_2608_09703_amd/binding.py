@@ -35,6 +35,7 @@ MLS_JUNCTION_ACCUMULATE = 1
 
 MLS_ACCUMULATE_GRAD_W = 1
 MLS_ACCUMULATE_GRAD_H = 2
+MLS_FWD_BWD_RECOMPUTE = 4
 
 MLS_DEVFLAG_LABEL_RANGE = 1
 MLS_DEVFLAG_NONFINITE = 2
@@ -43,6 +44,8 @@ EXPORTED = (
     "mls_query_sizes",
     "mls_distill_fwd",
     "mls_distill_bwd",
+    "mls_query_fwd_bwd_workspace",
+    "mls_distill_fwd_bwd",
     "mls_diagnostics",
     "mls_junction_fwd",
     "mls_junction_bwd",
@@ -134,6 +137,9 @@ def lib():
         L.mls_distill_fwd.argtypes = [P, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
         L.mls_distill_bwd.argtypes = [P, vp, vp, vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp,
                                       ctypes.c_size_t, vp]
+        L.mls_query_fwd_bwd_workspace.argtypes = [P, ctypes.POINTER(ctypes.c_size_t)]
+        L.mls_distill_fwd_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, ctypes.POINTER(vp),
+                                          ctypes.POINTER(vp), vp, ctypes.c_size_t, vp]
         L.mls_diagnostics.argtypes = [P, vp, vp, vp, vp, ctypes.c_size_t, vp]
         J = ctypes.POINTER(Junction)
         L.mls_junction_fwd.argtypes = [J, vp, vp, vp, vp]
@@ -225,6 +231,22 @@ def distill_bwd(p: Problem, stats: int, g_ce: Optional[int], g_kl: Optional[int]
     arr_W = (ctypes.c_void_p * MAX_MODELS)(*[x or None for x in grad_W])
     check(lib().mls_distill_bwd(ctypes.byref(p), stats, g_ce, g_kl, arr_h, arr_W, ws, ws_bytes,
                                 stream), "mls_distill_bwd")
+
+
+def query_fwd_bwd_workspace(p: Problem) -> int:
+    n = ctypes.c_size_t(0)
+    check(lib().mls_query_fwd_bwd_workspace(ctypes.byref(p), ctypes.byref(n)),
+          "mls_query_fwd_bwd_workspace")
+    return n.value
+
+
+def distill_fwd_bwd(p: Problem, stats: int, ce: int, kl: int, entropy: Optional[int],
+                    g_ce: Optional[int], g_kl: Optional[int], grad_h: Sequence[Optional[int]],
+                    grad_W: Sequence[Optional[int]], ws: int, ws_bytes: int, stream: int):
+    arr_h = (ctypes.c_void_p * MAX_MODELS)(*[x or None for x in grad_h])
+    arr_W = (ctypes.c_void_p * MAX_MODELS)(*[x or None for x in grad_W])
+    check(lib().mls_distill_fwd_bwd(ctypes.byref(p), stats, ce, kl, entropy, g_ce, g_kl, arr_h,
+                                    arr_W, ws, ws_bytes, stream), "mls_distill_fwd_bwd")
 
 
 def diagnostics(p: Problem, kl_pair: int, agree: int, argmax: Optional[int], ws: int,

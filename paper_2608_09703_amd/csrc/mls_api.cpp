@@ -84,6 +84,9 @@ inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 constexpr int64_t kSlabTargetBytes = 4ll << 30;  // logit-gradient slab(s) per chunk
 constexpr int64_t kMinChunks = 4;                 // the default plan never holds a [T, V] slab
+constexpr int64_t kRecordBudget = 1ll << 30;      // forward partial records of one token chunk
+constexpr int64_t kLogitSlabBudget = 16ll << 30;  // stored logits of one token chunk (all sub-models)
+constexpr int64_t kPanelMax = (1ll << 32) - 1;    // bytes one wide-GEMM operand may span
 
 struct Plan {
   int M = 0;
@@ -96,6 +99,18 @@ struct Plan {
   int64_t T_pad = 0;
   int n_tt = 0;
   int n_vt_fwd = 0;
+  // forward token chunks: the partial records of one chunk at a time
+  int64_t fwd_tc = 0;
+  int fwd_nc = 0;
+  // fused forward + backward (mls_distill_fwd_bwd): with fb_store, token chunks
+  // of fb_tc rows whose logits are stored (fp16, row length fb_ld) and turned
+  // into the logit gradient in place; otherwise the forward, then the
+  // recompute backward
+  bool fb_store = false;
+  int64_t fb_tc = 0;
+  int fb_nc = 0;
+  int64_t fb_ld = 0;
+  size_t fb_off_lslab = 0, fb_off_part = 0, fb_off_lab = 0, fb_bytes = 0;
   int64_t Vc = 0;
   int n_chunks = 0;
   // The wide gradient GEMM addresses its M-contiguous operands (the slab,
@@ -163,7 +178,6 @@ void make_plan(const mls_problem* p, Plan& pl) {
   pl.n_tt = (int)(pl.T_pad / kFusedBN);
   const int fbm = fused_tile_rows(pl.wide);
   pl.n_vt_fwd = (int)((p->V + fbm - 1) / fbm);
-  constexpr int64_t kPanelMax = (1ll << 32) - 1;  // bytes one wide-GEMM operand may span
   int64_t dmax = 0;
   for (int i = 0; i < p->M; ++i) dmax = std::max<int64_t>(dmax, p->d[i]);
   pl.wide_bwd = pl.wide && pl.T_pad * dmax * pl.es <= kPanelMax && pl.T_pad * 256 * pl.es <= kPanelMax;
@@ -190,9 +204,14 @@ void make_plan(const mls_problem* p, Plan& pl) {
   pl.n_chunks = (int)((p->V + pl.Vc - 1) / pl.Vc);
   pl.grad_h_bf16 = p->grad_h_dtype == MLS_BF16;
 
+  // forward: token chunks whose partial records stay within kRecordBudget
+  const int64_t rec_per_tok = (int64_t)pl.M * pl.n_vt_fwd * kFusedFwdParts * (int64_t)sizeof(float4);
+  pl.fwd_tc = std::min<int64_t>(pl.T_pad, std::max<int64_t>(kFusedBN, kRecordBudget / rec_per_tok /
+                                                                          kFusedBN * kFusedBN));
+  pl.fwd_nc = (int)((p->T + pl.fwd_tc - 1) / pl.fwd_tc);
   size_t off = 0;
   pl.off_partials = off;
-  off = align256(off + (size_t)pl.M * pl.n_vt_fwd * kFusedFwdParts * pl.T_pad * sizeof(float4));
+  off = align256(off + (size_t)rec_per_tok * pl.fwd_tc);
   pl.off_lab = off;
   off = align256(off + (size_t)pl.M * pl.T * sizeof(float));
   pl.fwd_bytes = off;
@@ -228,6 +247,38 @@ void make_plan(const mls_problem* p, Plan& pl) {
     pl.diag_bytes = off;
   }
   pl.ws_bytes = std::max(std::max(pl.fwd_bytes, pl.bwd_bytes), pl.diag_bytes);
+
+  // fused forward + backward with stored logits: at least two token chunks (so
+  // no [T, V] logits exist), each sub-model's fp16 slab below 4 GiB (the wide
+  // GEMM's 32-bit offsets) and all of them within kLogitSlabBudget; every head
+  // [V, d_i] must also fit one wide-GEMM operand
+  pl.fb_ld = (int64_t)pl.n_vt_fwd * kFusedBN;
+  const bool heads_fit = pl.V * dmax * pl.es <= kPanelMax;
+  pl.fb_store = pl.wide && p->T > kFusedBN && heads_fit && !(p->flags & MLS_FWD_BWD_RECOMPUTE);
+  if (pl.fb_store) {
+    const int64_t row = pl.fb_ld * 2;
+    int64_t cap = std::min<int64_t>(kPanelMax / row, kLogitSlabBudget / (row * pl.M));
+    cap = cap / kFusedBN * kFusedBN;
+    if (cap < kFusedBN) {
+      pl.fb_store = false;
+    } else {
+      const int64_t n = std::max<int64_t>(2, (p->T + cap - 1) / cap);
+      pl.fb_tc = round_up((p->T + n - 1) / n, kFusedBN);
+      pl.fb_nc = (int)((p->T + pl.fb_tc - 1) / pl.fb_tc);
+    }
+  }
+  if (pl.fb_store) {
+    off = 0;
+    pl.fb_off_lslab = off;
+    off = align256(off + (size_t)pl.M * pl.fb_tc * pl.fb_ld * 2);
+    pl.fb_off_part = off;
+    off = align256(off + (size_t)rec_per_tok * pl.fb_tc);
+    pl.fb_off_lab = off;
+    off = align256(off + (size_t)pl.M * pl.T * sizeof(float));
+    pl.fb_bytes = off;
+  } else {
+    pl.fb_bytes = std::max(pl.fwd_bytes, pl.bwd_bytes);
+  }
 
   pl.header_off = (size_t)(4ll * pl.M * pl.T + pl.T) * sizeof(float);
   pl.stats_bytes = align256(pl.header_off + 2 * sizeof(int32_t));
@@ -299,6 +350,72 @@ void host_coeffs(int M, int s, float alpha, float tau, int mode, const float* w,
       g_kl[i] = wi * alpha * tau * tau;
     }
   }
+}
+
+// Label logits of every token and, when `count` is set, the valid-token count
+// into the statistics header (which the logit-gradient pass reads before the
+// loss mean is taken).
+hipError_t launch_labels(const mls_problem* p, const Plan& pl, float* lab, void* stats, bool count,
+                         hipStream_t s) {
+  RowArgs r;
+  fill_rows(p, pl, r);
+  r.lab = lab;
+  r.header = reinterpret_cast<int32_t*>(static_cast<char*>(stats) + pl.header_off);
+  hipError_t e;
+  {
+    ProfScope ps("label_logits", s);
+    e = launch_label_logits(r, pl.f32, s);
+  }
+  if (e != hipSuccess || !count) return e;
+  ProfScope ps("count_valid", s);
+  return launch_count_valid(r, s);
+}
+
+// Forward of tokens [t0, t0 + tc): the tile kernel (partial records, and with
+// lslab the fp16 logits) and the row merge into the statistics.
+hipError_t forward_chunk(const mls_problem* p, const Plan& pl, int64_t t0, int64_t tc,
+                         float4* partials, const float* lab, uint16_t* lslab, void* stats,
+                         hipStream_t s) {
+  FusedArgs a;
+  fill_common(p, pl, a);
+  for (int i = 0; i < pl.M; ++i)
+    a.h[i] = static_cast<const char*>(p->h[i]) + (size_t)t0 * p->d[i] * pl.es;
+  a.T = tc;
+  a.n_tt = (int)((tc + kFusedBN - 1) / kFusedBN);
+  a.group_v = a.n_tt >= 64 ? 4 : 8;
+  a.n_vt = pl.n_vt_fwd;
+  a.partials = partials;
+  a.lslab = lslab;
+  a.ld_lslab = pl.fb_ld;
+  hipError_t e;
+  {
+    ProfScope ps("fused_fwd", s);
+    e = launch_fused_fwd(a, pl.f32, s);
+  }
+  if (e != hipSuccess) return e;
+  RowArgs r;
+  fill_rows(p, pl, r);
+  r.t0 = t0;
+  r.Tc = tc;
+  r.partials = partials;
+  r.lab = const_cast<float*>(lab);
+  r.stats = static_cast<float*>(stats);
+  ProfScope ps("row_merge", s);
+  return launch_finalize_rows(r, s);
+}
+
+// Means over the valid tokens, the valid count and the device flags.
+hipError_t finish_losses(const mls_problem* p, const Plan& pl, void* stats, float* ce, float* kl,
+                         float* entropy, hipStream_t s) {
+  RowArgs r;
+  fill_rows(p, pl, r);
+  r.stats = static_cast<float*>(stats);
+  r.header = reinterpret_cast<int32_t*>(static_cast<char*>(stats) + pl.header_off);
+  r.ce = ce;
+  r.kl = kl;
+  r.entropy = entropy;
+  ProfScope ps("loss_mean", s);
+  return launch_reduce_losses(r, s);
 }
 
 }  // namespace
@@ -390,41 +507,16 @@ mls_status mls_distill_fwd(const mls_problem* p, void* stats, float* ce, float* 
                 workspace_bytes);
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
-
-  FusedArgs a;
-  fill_common(p, pl, a);
-  a.n_vt = pl.n_vt_fwd;
-  a.partials = reinterpret_cast<float4*>(ws + pl.off_partials);
-  hipError_t e;
-  {
-    ProfScope ps("fused_fwd", s);
-    e = launch_fused_fwd(a, pl.f32, s);
-  }
-  if (e != hipSuccess) return hip_fail(e, "fused forward launch");
-
-  RowArgs r;
-  fill_rows(p, pl, r);
-  r.partials = a.partials;
-  r.lab = reinterpret_cast<float*>(ws + pl.off_lab);
-  r.stats = static_cast<float*>(stats);
-  r.header = reinterpret_cast<int32_t*>(static_cast<char*>(stats) + pl.header_off);
-  r.ce = ce;
-  r.kl = kl;
-  r.entropy = entropy;
-  {
-    ProfScope ps("label_logits", s);
-    e = launch_label_logits(r, pl.f32, s);
-  }
+  float* lab = reinterpret_cast<float*>(ws + pl.off_lab);
+  hipError_t e = launch_labels(p, pl, lab, stats, false, s);
   if (e != hipSuccess) return hip_fail(e, "label logits launch");
-  {
-    ProfScope ps("row_merge", s);
-    e = launch_finalize_rows(r, s);
+  for (int c = 0; c < pl.fwd_nc; ++c) {
+    const int64_t t0 = (int64_t)c * pl.fwd_tc;
+    e = forward_chunk(p, pl, t0, std::min(pl.fwd_tc, pl.T - t0),
+                      reinterpret_cast<float4*>(ws + pl.off_partials), lab, nullptr, stats, s);
+    if (e != hipSuccess) return hip_fail(e, "forward launch");
   }
-  if (e != hipSuccess) return hip_fail(e, "row merge launch");
-  {
-    ProfScope ps("loss_mean", s);
-    e = launch_reduce_losses(r, s);
-  }
+  e = finish_losses(p, pl, stats, ce, kl, entropy, s);
   if (e != hipSuccess) return hip_fail(e, "loss reduction launch");
   return MLS_OK;
 }
@@ -650,6 +742,166 @@ mls_status mls_distill_bwd(const mls_problem* p, const void* stats, const float*
     }
     if (e != hipSuccess) return hip_fail(e, "gradient GEMM launch");
   }
+  return MLS_OK;
+}
+
+mls_status mls_query_fwd_bwd_workspace(const mls_problem* p, size_t* workspace_bytes) {
+  g_last_error.clear();
+  mls_status st = validate(p);
+  if (st != MLS_OK) return st;
+  if (!workspace_bytes) return fail(MLS_INVALID_ARG, "workspace_bytes is NULL");
+  Plan pl;
+  make_plan(p, pl);
+  *workspace_bytes = pl.fb_bytes;
+  return MLS_OK;
+}
+
+mls_status mls_distill_fwd_bwd(const mls_problem* p, void* stats, float* ce, float* kl,
+                               float* entropy, const float* g_ce, const float* g_kl,
+                               void* const* grad_h, float* const* grad_W, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  mls_status st = validate(p);
+  if (st != MLS_OK) return st;
+  if (!stats || !ce || !kl || !workspace || !grad_h || !grad_W)
+    return fail(MLS_INVALID_ARG, "stats, ce, kl, workspace, grad_h and grad_W must be non-NULL");
+  if ((g_ce == nullptr) != (g_kl == nullptr))
+    return fail(MLS_INVALID_ARG, "g_ce and g_kl must both be given or both be NULL");
+  if (!aligned(stats, 16) || !aligned(workspace, 16) || !aligned(ce, 4) || !aligned(kl, 4))
+    return fail(MLS_INVALID_ARG, "misaligned stats / workspace / loss pointer");
+  for (int i = 0; i < p->M; ++i) {
+    if ((grad_h[i] && !aligned(grad_h[i], p->grad_h_dtype == MLS_BF16 ? 2 : 4)) ||
+        (grad_W[i] && !aligned(grad_W[i], 4)))
+      return fail(MLS_INVALID_ARG, "misaligned gradient pointer %d", i);
+  }
+  Plan pl;
+  make_plan(p, pl);
+  if (workspace_bytes < pl.fb_bytes)
+    return fail(MLS_WORKSPACE_TOO_SMALL, "forward + backward needs %zu workspace bytes, got %zu",
+                pl.fb_bytes, workspace_bytes);
+  if (!pl.fb_store) {
+    // one token tile, widths off the wide path, or the recompute plan asked for
+    st = mls_distill_fwd(p, stats, ce, kl, entropy, workspace, workspace_bytes, stream);
+    if (st != MLS_OK) return st;
+    return mls_distill_bwd(p, stats, g_ce, g_kl, grad_h, grad_W, workspace, workspace_bytes, stream);
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  float* lab = reinterpret_cast<float*>(ws + pl.fb_off_lab);
+  float4* part = reinterpret_cast<float4*>(ws + pl.fb_off_part);
+  uint16_t* lslab = reinterpret_cast<uint16_t*>(ws + pl.fb_off_lslab);
+  hipError_t e = launch_labels(p, pl, lab, stats, true, s);
+  if (e != hipSuccess) return hip_fail(e, "label logits launch");
+
+  GradArgs ga;
+  memset(&ga, 0, sizeof(ga));
+  ga.M = pl.M;
+  fill_order(pl, ga.order);
+  ga.T = pl.T;
+  ga.V = pl.V;
+  ga.ld = pl.fb_ld;
+  ga.labels = p->labels;
+  ga.ignore_index = p->ignore_index;
+  ga.inv_tau = 1.0f / p->tau;
+  const float* sf = static_cast<const float*>(stats);
+  ga.lse1 = sf;
+  ga.lset = sf + (int64_t)pl.M * pl.T;
+  ga.n_valid = reinterpret_cast<const int32_t*>(static_cast<const char*>(stats) + pl.header_off);
+  ga.g_ce = g_ce;
+  ga.g_kl = g_kl;
+  host_coeffs(pl.M, pl.s, p->alpha, p->tau, MLS_MODE_PAPER, nullptr, ga.host_gce, ga.host_gkl);
+  ga.partials = part;
+  ga.n_rec = pl.n_vt_fwd * kFusedFwdParts;
+  ga.slab = lslab;
+
+  const int64_t kt = gemm_wide_k_tile();
+  const int tbm = gemm_tile_rows(true);
+  const int tbn = gemm_tile_cols(true);
+  for (int c = 0; c < pl.fb_nc; ++c) {
+    const int64_t t0 = (int64_t)c * pl.fb_tc;
+    const int64_t tc = std::min(pl.fb_tc, pl.T - t0);
+    const int64_t tc_pad = round_up(tc, kFusedBN);
+    e = forward_chunk(p, pl, t0, tc, part, lab, lslab, stats, s);
+    if (e != hipSuccess) return hip_fail(e, "forward launch");
+
+    ga.Tc = tc;
+    ga.Tc_pad = tc_pad;
+    ga.t0 = t0;
+    {
+      ProfScope ps("grad_logits", s);
+      e = launch_grad_logits(ga, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "logit gradient launch");
+
+    // grad_h_i[chunk rows] = G_i W_i (K = V, complete in this chunk) and
+    // grad_W_i (+)= G_i^T h_i[chunk rows] (K = the chunk's tokens), one launch
+    const size_t slab_stride = (size_t)tc_pad * pl.fb_ld * 2;
+    GemmArgs gm;
+    memset(&gm, 0, sizeof(gm));
+    int tiles = 0;
+    for (int i = 0; i < pl.M; ++i) {
+      if (!grad_h[i]) continue;
+      GemmGroup& g = gm.g[gm.ngroups++];
+      g.A = reinterpret_cast<const char*>(lslab) + (size_t)i * slab_stride;  // [t][v]
+      g.lda = pl.fb_ld;
+      g.rows = tc;
+      g.B = p->W[i];  // [v][d]
+      g.ldb = p->d[i];
+      g.cols = pl.V;
+      if (pl.grad_h_bf16)
+        g.Cb = static_cast<uint16_t*>(grad_h[i]) + t0 * p->d[i];
+      else
+        g.C = static_cast<float*>(grad_h[i]) + t0 * p->d[i];
+      g.accumulate = (p->flags & MLS_ACCUMULATE_GRAD_H) ? 1 : 0;
+      g.ldc = p->d[i];
+      g.ldc_rows = tc;
+      g.K = round_up(pl.V, kt);
+      g.kind = 0;
+      g.tiles_m = (int)((tc + tbm - 1) / tbm);
+      g.tiles_n = (int)((p->d[i] + tbn - 1) / tbn);
+      g.tile_begin = tiles;
+      g.group_m = 8;
+      tiles += g.tiles_m * g.tiles_n;
+    }
+    const int grad_h_tiles = tiles;
+    for (int i = 0; i < pl.M; ++i) {
+      if (!grad_W[i]) continue;
+      GemmGroup& g = gm.g[gm.ngroups++];
+      g.A = reinterpret_cast<const char*>(lslab) + (size_t)i * slab_stride;  // [t][v] as [k][m]
+      g.lda = pl.fb_ld;
+      g.rows = tc_pad;
+      g.B = static_cast<const char*>(p->h[i]) + (size_t)t0 * p->d[i] * pl.es;  // [t][d]
+      g.ldb = p->d[i];
+      g.cols = tc;
+      g.C = grad_W[i];
+      g.ldc = p->d[i];
+      g.ldc_rows = pl.V;
+      g.K = tc_pad;
+      g.kind = 1;
+      g.tiles_m = (int)((pl.V + tbm - 1) / tbm);
+      g.tiles_n = (int)((p->d[i] + tbn - 1) / tbn);
+      g.tile_begin = tiles;
+      g.accumulate = (c > 0 || (p->flags & MLS_ACCUMULATE_GRAD_W)) ? 1 : 0;
+      g.group_m = 0;
+      tiles += g.tiles_m * g.tiles_n;
+    }
+    gm.phase_tiles = 0;
+    if (grad_h_tiles > 0 && grad_h_tiles < tiles) {
+      bool fits = true;
+      for (int x = 0; x < 8; ++x) {
+        const int q1 = grad_h_tiles / 8 + (x < grad_h_tiles % 8 ? 1 : 0);
+        if (q1 > (tiles - x + 7) / 8) fits = false;
+      }
+      if (fits) gm.phase_tiles = grad_h_tiles;
+    }
+    {
+      ProfScope ps("gemm_grads", s);
+      e = launch_gemm_wide(gm, tiles, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "gradient GEMM launch");
+  }
+  e = finish_losses(p, pl, stats, ce, kl, entropy, s);
+  if (e != hipSuccess) return hip_fail(e, "loss reduction launch");
   return MLS_OK;
 }
 

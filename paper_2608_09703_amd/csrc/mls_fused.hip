@@ -69,7 +69,11 @@ struct TeacherTile<FM, FN, true> {
 // (max, sum exp, sum exp at tau, teacher-weighted logit sum) per token and wave
 // row. Each wave normalises to the max over its own rows, so the epilogue needs
 // no exchange between waves; the row merge rescales the records.
-template <class Mma, typename E, bool TAU1, int MINB = 1>
+// STORE (fused forward + backward): every logit also goes to the chunk's slab as
+// fp16 of its distance to the record's maximum (at most 0; 2^-11 relative, so
+// the entries that carry the softmax's mass, near the maximum, are the most
+// exact), token-major, for the logit gradient pass.
+template <class Mma, typename E, bool TAU1, int MINB = 1, bool STORE = false>
 __global__ __launch_bounds__(Mma::NT, MINB) void fused_fwd_kernel(FusedArgs a) {
   constexpr int BM = Mma::kBM;
   constexpr int BN = Mma::kBN;
@@ -120,6 +124,28 @@ __global__ __launch_bounds__(Mma::NT, MINB) void fused_fwd_kernel(FusedArgs a) {
           if (ok) mb = fmaxf(mb, mma.acc[fm][fn][r]);
         }
       mb = fmaxf(mb, shfl_xor32(mb));
+
+      if constexpr (STORE) {
+        // four consecutive vocabulary rows of one token per 8-byte store; the
+        // two lane halves fill 16 contiguous bytes, a wave's 64 rows one
+        // 128-byte line per token
+        const int c = Mma::col_of(wn, fn, lane);
+        uint16_t* row = a.lslab + ((int64_t)i * a.n_tt * BN + tbase + c) * a.ld_lslab + vbase;
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+          for (int rg = 0; rg < 4; ++rg) {
+            uint32_t w[2];
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+              const float x0 = mma.acc[fm][fn][rg * 4 + 2 * k] - mb;
+              const float x1 = mma.acc[fm][fn][rg * 4 + 2 * k + 1] - mb;
+              w[k] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)x0) |
+                     ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)x1) << 16);
+            }
+            *reinterpret_cast<uint2*>(row + Mma::row_of(wm, fm, rg * 4, lane)) = make_uint2(w[0], w[1]);
+          }
+      }
 
       // 2. sums relative to that max (every term is 0 on rows beyond V)
       float s1 = 0.f, st = 0.f, xr = 0.f;
@@ -424,14 +450,23 @@ hipError_t launch_fused_fwd(const FusedArgs& a, bool f32, hipStream_t stream) {
                 : launch_fwd_t<GenMmaF32, F32, false>(a, stream);
   if (a.wide) {
     dim3 grid((unsigned)a.n_tt * (unsigned)a.n_vt);
-    if (tau1)
+    if (a.lslab) {
+      if (tau1)
+        hipLaunchKernelGGL((fused_fwd_kernel<WideFused, Bf16, true, 2, true>), grid,
+                           dim3(WideFused::NT), 0, stream, a);
+      else
+        hipLaunchKernelGGL((fused_fwd_kernel<WideFused, Bf16, false, 2, true>), grid,
+                           dim3(WideFused::NT), 0, stream, a);
+    } else if (tau1) {
       hipLaunchKernelGGL((fused_fwd_kernel<WideFused, Bf16, true, 2>), grid, dim3(WideFused::NT), 0,
                          stream, a);
-    else
+    } else {
       hipLaunchKernelGGL((fused_fwd_kernel<WideFused, Bf16, false, 2>), grid, dim3(WideFused::NT), 0,
                          stream, a);
+    }
     return hipGetLastError();
   }
+  if (a.lslab) return hipErrorInvalidValue;  // the stored-logit forward is wide-only
   return tau1 ? launch_fwd_t<GenMmaBf16, Bf16, true>(a, stream)
               : launch_fwd_t<GenMmaBf16, Bf16, false>(a, stream);
 }

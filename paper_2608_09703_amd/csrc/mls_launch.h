@@ -50,6 +50,10 @@ struct FusedArgs {
   int32_t n_vt;  // vocabulary tiles in this launch
   // forward
   float4* partials;  // [M (processing order)][n_tt][n_vt * kFusedFwdParts][kFusedBN]
+  // forward of the fused forward + backward: every logit, as fp16 of its
+  // distance to its partial record's maximum, [M (sub-model index)][n_tt * BN][ld_lslab]
+  uint16_t* lslab;
+  int64_t ld_lslab;
   // backward
   const float* lse1;  // [M][T]
   const float* lset;  // [M][T]
@@ -135,13 +139,43 @@ struct RowArgs {
   float tau;
   int32_t order[kMaxModels];  // sub-model of each partial slot; order[0] is the teacher
   int32_t n_rec;           // partial records per token and sub-model
-  const float4* partials;  // [M slots][ceil(T / kFusedBN)][n_rec][kFusedBN]
+  // row merge: the forward chunk of tokens [t0, t0 + Tc) whose records follow
+  int64_t t0;
+  int64_t Tc;
+  const float4* partials;  // [M slots][ceil(Tc / kFusedBN)][n_rec][kFusedBN]
   float* lab;              // [M][T] label logits
   float* stats;            // lse1, lset, ce_row, kl_row, h_row
   int32_t* header;         // n_valid, flags
   float* ce;
   float* kl;
   float* entropy;
+};
+
+// Logit gradient of one token chunk from its stored logits (fused forward +
+// backward): the slab holds fp16 l - m (m: the partial record's maximum) and
+// receives bf16 G in place.
+struct GradArgs {
+  int32_t M;
+  int32_t order[kMaxModels];  // processing order of the records; order[0] is the teacher
+  int64_t Tc;                 // tokens of the chunk (rows of the slab with data)
+  int64_t Tc_pad;             // rows of each sub-model's slab
+  int64_t t0;                 // first token of the chunk
+  int64_t T;                  // all tokens (statistics row length)
+  int64_t V;
+  int64_t ld;                 // slab row length (>= V, a multiple of 8)
+  const int64_t* labels;      // [T]
+  int64_t ignore_index;
+  float inv_tau;
+  const float* lse1;          // [M][T]
+  const float* lset;          // [M][T]
+  const int32_t* n_valid;
+  const float* g_ce;          // device [M] or null (host values then)
+  const float* g_kl;
+  float host_gce[kMaxModels];
+  float host_gkl[kMaxModels];
+  const float4* partials;     // [M slots][Tc_pad / kFusedBN][n_rec][kFusedBN]
+  int32_t n_rec;
+  uint16_t* slab;             // [M][Tc_pad][ld]
 };
 
 // Cross-model diagnostics (M <= kMaxDiagModels).
@@ -275,5 +309,7 @@ hipError_t launch_verify(const VerifyArgs& a, int ept, hipStream_t stream);
 hipError_t launch_label_logits(const RowArgs& a, bool f32, hipStream_t stream);
 hipError_t launch_finalize_rows(const RowArgs& a, hipStream_t stream);
 hipError_t launch_reduce_losses(const RowArgs& a, hipStream_t stream);
+hipError_t launch_count_valid(const RowArgs& a, hipStream_t stream);
+hipError_t launch_grad_logits(const GradArgs& a, hipStream_t stream);
 
 }  // namespace mls

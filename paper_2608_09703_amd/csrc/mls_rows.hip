@@ -86,12 +86,14 @@ constexpr int kRowGrp = 16;   // partial groups per token, merged pairwise in a 
 static_assert(kRowTok * kRowGrp == kThreads && (kRowGrp & (kRowGrp - 1)) == 0, "row merge shape");
 static_assert(kFusedBN % kRowTok == 0, "a block's tokens lie in one token tile");
 
+// Tokens [t0, t0 + Tc) of one forward chunk: its partial records are indexed
+// by the token inside the chunk, the statistics by the token itself.
 template <int MM>
 __global__ __launch_bounds__(kThreads) void finalize_rows_kernel(RowArgs a) {
   __shared__ float4 sh[kRowGrp][kRowTok][MM];
   const int tl = threadIdx.x % kRowTok;
   const int grp = threadIdx.x / kRowTok;
-  const int64_t t = (int64_t)blockIdx.x * kRowTok + tl;
+  const int64_t tc = (int64_t)blockIdx.x * kRowTok + tl;  // token inside the chunk
   const float inv_tau = 1.0f / a.tau;
   const float ct = kLog2e * inv_tau;
 
@@ -103,9 +105,9 @@ __global__ __launch_bounds__(kThreads) void finalize_rows_kernel(RowArgs a) {
     st.st[i] = 0.f;
     st.xr[i] = 0.f;
   }
-  if (t < a.T) {
-    const int64_t n_tt = (a.T + kFusedBN - 1) / kFusedBN;
-    const float4* part = a.partials + (t / kFusedBN) * a.n_rec * kFusedBN + t % kFusedBN;
+  if (tc < a.Tc) {
+    const int64_t n_tt = (a.Tc + kFusedBN - 1) / kFusedBN;
+    const float4* part = a.partials + (tc / kFusedBN) * a.n_rec * kFusedBN + tc % kFusedBN;
 #pragma unroll 4
     for (int j = grp; j < a.n_rec; j += kRowGrp) {
       float4 rec[MM];
@@ -135,8 +137,9 @@ __global__ __launch_bounds__(kThreads) void finalize_rows_kernel(RowArgs a) {
       }
     }
   }
-  if (grp != 0 || t >= a.T) return;
+  if (grp != 0 || tc >= a.Tc) return;
 
+  const int64_t t = a.t0 + tc;
   const int64_t y = a.labels[t];
   const bool valid = y != a.ignore_index && y >= 0 && y < a.V;
   const int64_t T = a.T;
@@ -226,7 +229,126 @@ __global__ __launch_bounds__(kRedThreads) void reduce_losses_kernel(RowArgs a) {
                 (finite ? 0 : MLS_DEVFLAG_NONFINITE);
 }
 
+// Number of valid tokens into the statistics header (the fused forward +
+// backward needs it before the loss mean is taken).
+__global__ __launch_bounds__(kRedThreads) void count_valid_kernel(RowArgs a) {
+  __shared__ int part[kRedThreads / 64];
+  int n = 0;
+  for (int64_t t = threadIdx.x; t < a.T; t += kRedThreads) {
+    const int64_t y = a.labels[t];
+    n += (y != a.ignore_index && y >= 0 && y < a.V) ? 1 : 0;
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) n += __shfl_xor(n, o, 64);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = n;
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  int tot = 0;
+  for (int w = 0; w < kRedThreads / 64; ++w) tot += part[w];
+  a.header[0] = tot;
+}
+
+// Logit gradient of one token chunk from its stored logits, in place:
+//   G_i = ( g_ce,i (softmax(l_i) - onehot(y)) + g_kl,i / tau (softmax(l_i / tau) - q) ) / N
+// (eq. (2) with stop_grad on q = softmax(l_s / tau), eq. (3) through the
+// coefficients), with l = m + d rebuilt from the stored fp16 distance d to the
+// partial record's maximum m. One wave per token row, 8 vocabulary entries per
+// lane (16-byte loads and stores), the teacher first so that its q stays in
+// registers for the students. Ignored tokens, padding rows and entries past V
+// get exact zeros.
+constexpr int kGradTok = 4;    // token rows per block, one per wave
+constexpr int kGradSpan = 512; // vocabulary entries per wave
+
+__device__ __forceinline__ void unpack_f16x8(uint4 v, float* d) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    d[2 * k] = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[k] & 0xffffu));
+    d[2 * k + 1] = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[k] >> 16));
+  }
+}
+
+__device__ __forceinline__ uint4 pack_bf16x8(const float* g) {
+  uint32_t w[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    w[k] = (uint32_t)to_storage<Bf16>(g[2 * k]) | ((uint32_t)to_storage<Bf16>(g[2 * k + 1]) << 16);
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+template <bool TAU1>
+__global__ __launch_bounds__(kThreads) void grad_logits_kernel(GradArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t tc = (int64_t)blockIdx.y * kGradTok + wave;
+  const int64_t v0 = (int64_t)blockIdx.x * kGradSpan + (int64_t)lane * 8;
+  if (tc >= a.Tc_pad || v0 >= a.ld) return;  // no barrier follows
+  const int64_t stride = a.Tc_pad * a.ld;
+  const int64_t t = a.t0 + tc;
+  int64_t y = tc < a.Tc ? a.labels[t] : a.ignore_index;
+  const bool valid = tc < a.Tc && y != a.ignore_index && y >= 0 && y < a.V;
+  if (!valid) {
+    for (int oi = 0; oi < a.M; ++oi)
+      *reinterpret_cast<uint4*>(a.slab + a.order[oi] * stride + tc * a.ld + v0) = make_uint4(0, 0, 0, 0);
+    return;
+  }
+  const int nv = *a.n_valid;
+  const float invN = nv > 0 ? 1.0f / (float)nv : 0.0f;
+  const int yrel = (int)(y - v0);  // onehot position among this lane's 8 entries, if in [0, 8)
+  const float ct = kLog2e * a.inv_tau;
+  // partial record of this token and 64-entry group, for each slot
+  const int64_t slot = (a.Tc_pad / kFusedBN) * a.n_rec * kFusedBN;
+  const float4* rec = a.partials + ((tc / kFusedBN) * a.n_rec + v0 / 64) * kFusedBN + tc % kFusedBN;
+  float q[8];
+  for (int oi = 0; oi < a.M; ++oi) {
+    const int i = a.order[oi];
+    uint16_t* ptr = a.slab + i * stride + tc * a.ld + v0;
+    float d[8];
+    unpack_f16x8(*reinterpret_cast<const uint4*>(ptr), d);
+    const float m = rec[oi * slot].x;
+    const float l1s = a.lse1[(int64_t)i * a.T + t] * kLog2e;
+    const float lts = a.lset[(int64_t)i * a.T + t] * kLog2e;
+    const float gce = a.g_ce ? a.g_ce[i] : a.host_gce[i];
+    const float gkl = a.g_kl ? a.g_kl[i] : a.host_gkl[i];
+    const float cg = gce * invN;
+    const float ck = oi != 0 ? gkl * invN * a.inv_tau : 0.f;
+    float g[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const bool ok = v0 + j < a.V;
+      const float l = d[j] + m;
+      const float oh = j == yrel ? 1.f : 0.f;
+      if (oi == 0) {
+        const float qj = ok ? fast_exp2(fmaf(l, ct, -lts)) : 0.f;
+        q[j] = qj;
+        const float p1 = TAU1 ? qj : (ok ? fast_exp2(fmaf(l, kLog2e, -l1s)) : 0.f);
+        g[j] = cg * (p1 - oh);
+      } else {
+        const float p1 = ok ? fast_exp2(fmaf(l, kLog2e, -l1s)) : 0.f;
+        const float pt = TAU1 ? p1 : (ok ? fast_exp2(fmaf(l, ct, -lts)) : 0.f);
+        g[j] = fmaf(cg, p1 - oh, ck * (pt - q[j]));
+      }
+      g[j] = ok ? g[j] : 0.f;
+    }
+    *reinterpret_cast<uint4*>(ptr) = pack_bf16x8(g);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_count_valid(const RowArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(count_valid_kernel, dim3(1), dim3(kRedThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_grad_logits(const GradArgs& a, hipStream_t stream) {
+  dim3 grid((unsigned)((a.ld + kGradSpan - 1) / kGradSpan), (unsigned)((a.Tc_pad + kGradTok - 1) / kGradTok));
+  if (a.inv_tau == 1.0f)
+    hipLaunchKernelGGL(grad_logits_kernel<true>, grid, dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(grad_logits_kernel<false>, grid, dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_label_logits(const RowArgs& a, bool f32, hipStream_t stream) {
   const int64_t waves = (int64_t)a.M * a.T;
@@ -240,7 +362,7 @@ hipError_t launch_label_logits(const RowArgs& a, bool f32, hipStream_t stream) {
 
 template <int MM>
 hipError_t launch_finalize_rows_m(const RowArgs& a, hipStream_t stream) {
-  dim3 grid((unsigned)((a.T + kRowTok - 1) / kRowTok));
+  dim3 grid((unsigned)((a.Tc + kRowTok - 1) / kRowTok));
   hipLaunchKernelGGL(finalize_rows_kernel<MM>, grid, dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }

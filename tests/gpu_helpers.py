@@ -51,6 +51,41 @@ def run_gpu(h, W, labels, *, tau=1.0, teacher=-1, g_ce=None, g_kl=None, vocab_ch
     return out
 
 
+def run_fused(h, W, labels, *, tau=1.0, teacher=-1, g_ce=None, g_kl=None, alpha=0.0, flags=0,
+              grad_h_dtype=torch.float32, vocab_chunk=0):
+    """mls_distill_fwd_bwd through the C ABI; the same dict as run_gpu."""
+    from paper_2608_09703_amd import binding as B
+    dev = h[0].device
+    p = D.make_problem(h, W, labels, tau=tau, teacher=teacher, alpha=alpha, flags=flags,
+                       grad_h_dtype=grad_h_dtype, vocab_chunk=vocab_chunk)
+    buf = D.Buffers(p, dev)
+    ws_b = B.query_fwd_bwd_workspace(p)
+    ws = torch.empty(max(ws_b, 256), dtype=torch.uint8, device=dev)
+    gh = [torch.full(x.shape, float("nan"), dtype=grad_h_dtype, device=dev) for x in h]
+    gW = [torch.full(x.shape, float("nan"), dtype=torch.float32, device=dev) for x in W]
+    gce = torch.tensor(g_ce, dtype=torch.float32, device=dev) if g_ce is not None else None
+    gkl = torch.tensor(g_kl, dtype=torch.float32, device=dev) if g_kl is not None else None
+    st = torch.cuda.current_stream(dev).cuda_stream
+    B.distill_fwd_bwd(p, buf.stats.data_ptr(), buf.ce.data_ptr(), buf.kl.data_ptr(),
+                      buf.entropy.data_ptr(), gce.data_ptr() if gce is not None else None,
+                      gkl.data_ptr() if gkl is not None else None, [x.data_ptr() for x in gh],
+                      [x.data_ptr() for x in gW], ws.data_ptr(), ws_b, st)
+    M, T = len(h), h[0].shape[0]
+    lse1, lset, ce_row, kl_row, h_row = buf.stats_view(M, T)
+    out = {
+        "ce": buf.ce.cpu().numpy().astype(np.float64),
+        "kl": buf.kl.cpu().numpy().astype(np.float64),
+        "H": float(buf.entropy.cpu().numpy()[0]),
+        "lse1": lse1.cpu().numpy(), "lset": lset.cpu().numpy(), "ce_row": ce_row.cpu().numpy(),
+        "kl_row": kl_row.cpu().numpy(), "h_row": h_row.cpu().numpy(),
+        "grad_h": [x.float().cpu().numpy() for x in gh],
+        "grad_W": [x.cpu().numpy() for x in gW],
+        "ws_bytes": ws_b,
+    }
+    out["n_valid"], out["flags"] = B.read_stats_header(p, buf.stats.data_ptr(), st)
+    return out
+
+
 def assert_losses(gpu, ref, what=""):
     for k in ("ce", "kl"):
         np.testing.assert_allclose(gpu[k], ref[k], rtol=LOSS_RTOL, atol=LOSS_ATOL,

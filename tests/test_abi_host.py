@@ -351,3 +351,23 @@ def test_decode_entry_points_reject_bad_arguments_before_device_work():
         B.head_logits(102, 49152, 1024, B.MLS_BF16, fake + 8, fake + (1 << 32), fake + (2 << 32),
                       None)
     assert e.value.status == B.MLS_INVALID_ARG
+
+
+def test_fused_plan_never_holds_a_full_logit_array():
+    """mls_distill_fwd_bwd stores logits one token chunk at a time: at least two
+    chunks, each sub-model's fp16 chunk below 4 GiB, all of them within 16 GiB."""
+    for (M, T, dims, V) in [(3, 4096, [1024, 2048, 3072], 50304),
+                            (3, 8192, [1024, 2048, 3072], 128256),
+                            (4, 16384, [512, 1024, 2048, 4096], 128256),
+                            (3, 32768, [1536, 3072, 4608], 262144)]:
+        p = _fake_problem(M=M, T=T, dims=dims, V=V)
+        ws = B.query_fwd_bwd_workspace(p)
+        V_pad = (V + 127) // 128 * 128
+        full = M * T * V_pad * 2
+        assert ws < full // 2 + (1 << 30), (T, V, ws)
+        tc_max = ((1 << 32) - 1) // (V_pad * 2) // 128 * 128
+        assert ws >= M * min(tc_max, (T + 1) // 2) * V_pad * 2 * 0.9 or ws >= (1 << 30)
+        assert ws <= (16 << 30) + (2 << 30)
+    # one 128-token tile: the forward and the recomputing backward
+    p = _fake_problem(M=2, T=100, dims=[64, 128], V=1000)
+    assert B.query_fwd_bwd_workspace(p) <= B.query_sizes(p)[0]
