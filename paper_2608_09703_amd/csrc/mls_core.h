@@ -25,6 +25,20 @@ namespace mls {
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void glb_void_t;
 
+// Buffer descriptor of a block-uniform base and byte count. The inputs pass
+// through readfirstlane so the descriptor lives in scalar registers: values
+// the compiler derived with vector instructions (tile coordinates from integer
+// division) would otherwise leave it in vector registers, and every buffer
+// load through it would then be wrapped in a loop over distinct descriptors.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const char* base, int bytes) {
+  const uint64_t v = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  void* p = reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, __builtin_amdgcn_readfirstlane(bytes),
+                                           0x00020000);
+}
+
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
@@ -200,8 +214,7 @@ struct WideMma {
                                                                          int64_t ld_bytes,
                                                                          int64_t m0, int64_t nrows) {
     const int64_t bytes = nrows * ld_bytes - m0 * 2;
-    return __builtin_amdgcn_make_buffer_rsrc((void*)(base + m0 * 2), (short)0,
-                                             (int)(bytes > 0 ? bytes : 0), 0x00020000);
+    return uniform_rsrc(base + m0 * 2, (int)(bytes > 0 ? bytes : 0));
   }
 
   __device__ __forceinline__ static __amdgpu_buffer_rsrc_t panel_rsrc(const char* base,
@@ -211,8 +224,7 @@ struct WideMma {
     int64_t avail = nrows - row0;
     avail = avail < rows ? avail : rows;
     avail = avail > 0 ? avail : 0;
-    return __builtin_amdgcn_make_buffer_rsrc((void*)(base + row0 * ld_bytes), (short)0,
-                                             (int)(avail * ld_bytes), 0x00020000);
+    return uniform_rsrc(base + row0 * ld_bytes, (int)(avail * ld_bytes));
   }
 
   // Enqueue the direct loads of one operand tile. `vofs` is added to every

@@ -128,7 +128,9 @@ __global__ __launch_bounds__(Mma::NT, MINB) void fused_fwd_kernel(FusedArgs a) {
       if constexpr (STORE) {
         // four consecutive vocabulary rows of one token per 8-byte store; the
         // two lane halves fill 16 contiguous bytes, a wave's 64 rows one
-        // 128-byte line per token
+        // 128-byte line per token (staging through LDS for whole-line stores
+        // needs 16 KB more per block, which costs the second block per CU:
+        // slower)
         const int c = Mma::col_of(wn, fn, lane);
         uint16_t* row = a.lslab + ((int64_t)i * a.n_tt * BN + tbase + c) * a.ld_lslab + vbase;
 #pragma unroll

@@ -90,18 +90,63 @@ __device__ __forceinline__ void wide_tile(const GemmGroup& g, int tm, int tn, in
   Mma mma;
   mma.run(static_cast<const char*>(g.A), g.lda * 2, m0, g.rows, static_cast<const char*>(g.B),
           g.ldb * 2, n0, g.cols, g.K * 2, smem, tid);
+  // Epilogue through buffer descriptors over the tile's rows [m0, m0 + BM)
+  // that exist (rows past mext fall outside them: their loads return 0 and
+  // their stores are dropped), so each element's address is a 32-bit offset.
+  // One column block (FM x 32 x 32 values per wave) at a time: every value to
+  // add to it (the old output, or the partial sums of earlier chunks) is loaded
+  // before any is used, so a read-modify-write tile waits for memory FN times
+  // rather than once per 32 x 32 block.
+  const int64_t rows = mext - m0 < Mma::kBM ? mext - m0 : Mma::kBM;
+  const bool out16 = g.Cb != nullptr;
+  const int es = out16 ? 2 : 4;
+  const __amdgpu_buffer_rsrc_t rc =
+      out16 ? uniform_rsrc(reinterpret_cast<const char*>(g.Cb + m0 * g.ldc), (int)(rows * g.ldc * 2))
+            : uniform_rsrc(reinterpret_cast<const char*>(g.C + m0 * g.ldc), (int)(rows * g.ldc * 4));
+  const bool part = out16 && g.Cpart;
+  const __amdgpu_buffer_rsrc_t rp =
+      uniform_rsrc(reinterpret_cast<const char*>(part ? g.Cpart + m0 * g.ldc : g.C), part ? (int)(rows * g.ldc * 4) : 0);
+  const bool acc_old = g.accumulate != 0;
+  const int ldc = (int)g.ldc;
 #pragma unroll
-  for (int fm = 0; fm < FM; ++fm)
+  for (int fn = 0; fn < FN; ++fn) {
+    const int col = (int)n0 + Mma::col_of(wn, fn, lane);
+    const bool colok = col < next;
+    float add[FM][16];
+    if (acc_old || part) {
 #pragma unroll
-    for (int fn = 0; fn < FN; ++fn) {
-      const int64_t n = n0 + Mma::col_of(wn, fn, lane);
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int e = Mma::row_of(wm, fm, r, lane) * ldc + col;
+          float v = 0.f;
+          if (colok) {
+            if (part) v = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rp, e * 4, 0, 0));
+            if (acc_old) {
+              if (out16)
+                v += __uint_as_float((uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rc, e * 2, 0, 0) << 16);
+              else
+                v += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rc, e * 4, 0, 0));
+            }
+          }
+          add[fm][r] = v;
+        }
+    }
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int64_t m = m0 + Mma::row_of(wm, fm, r, lane);
-        if (m < mext && n < next) store_out(g, m * g.ldc + n, mma.acc[fm][fn][r]);
+        const int e = Mma::row_of(wm, fm, r, lane) * ldc + col;
+        const float v = mma.acc[fm][fn][r] + ((acc_old || part) ? add[fm][r] : 0.f);
+        if (colok) {
+          if (out16)
+            __builtin_amdgcn_raw_buffer_store_b16(to_storage<Bf16>(v), rc, e * es, 0, 0);
+          else
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), rc, e * es, 0, 0);
+        }
       }
-      __builtin_amdgcn_sched_barrier(0);  // one 32x32 block of stores at a time
-    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
 }
 
 template <class MmaH, class MmaW>

@@ -81,8 +81,8 @@ __device__ __forceinline__ void absorb(RowState<MM>& st, float ct, const float4*
   }
 }
 
-constexpr int kRowTok = 16;   // tokens per block
-constexpr int kRowGrp = 16;   // partial groups per token, merged pairwise in a fixed tree
+constexpr int kRowTok = 8;    // tokens per block
+constexpr int kRowGrp = 32;   // partial groups per token, merged pairwise in a fixed tree
 static_assert(kRowTok * kRowGrp == kThreads && (kRowGrp & (kRowGrp - 1)) == 0, "row merge shape");
 static_assert(kFusedBN % kRowTok == 0, "a block's tokens lie in one token tile");
 
