@@ -340,11 +340,25 @@ struct WideMma {
                                       const char* __restrict__ B, int64_t ldb_bytes,
                                       int64_t b_row0, int64_t b_rows, int64_t kbytes,
                                       char* smem, int tid) {
+    run_from(A, lda_bytes, a_row0, a_rows, B, ldb_bytes, b_row0, b_rows, kbytes, smem, tid,
+             [this]() { zero(); });
+  }
+
+  // As run(), with the accumulators set by init() instead of zeroed. init()
+  // runs before any K-tile load is issued, so loads it issues are older than
+  // the first K-tile's and are complete once that K-tile is (loads return in
+  // order): their latency hides behind the pipeline's prologue.
+  template <class Init>
+  __device__ __forceinline__ void run_from(const char* __restrict__ A, int64_t lda_bytes,
+                                           int64_t a_row0, int64_t a_rows,
+                                           const char* __restrict__ B, int64_t ldb_bytes,
+                                           int64_t b_row0, int64_t b_rows, int64_t kbytes,
+                                           char* smem, int tid, Init&& init) {
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int wm = wave % WGM;
     const int wn = wave / WGM;
-    zero();
+    init();
     const int nk = (int)(kbytes / RB);
     // KC operands: panel of BM (BN) rows, K position as scalar byte offset.
     // MC operands: panel of BM (BN) columns, K position as scalar row offset.

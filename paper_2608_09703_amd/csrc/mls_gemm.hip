@@ -76,6 +76,126 @@ constexpr int kWideBN = 256;
 using WideGemmH = WideMma<kWideBM, kWideBN, 2, 4, 2, 128, kLayoutKC, kLayoutMC, true>;
 using WideGemmW = WideMma<kWideBM, kWideBN, 2, 4, 2, 128, kLayoutMC, kLayoutMC, true>;
 
+// Loads and stores of one wave's part of an output tile through buffer
+// descriptors over the tile's existing rows (rows past them read as 0 and are
+// not written). Element (row, col) of the tile is at byte offset
+// (row * ldc + col) * size; coff[fn] is the lane's part for column block fn,
+// (its first row) * ldc + its column. A wave's 32-column block lies wholly
+// inside or outside the output (widths are multiples of 64), so blocks past it
+// are skipped by a uniform branch (ok[fn]). INSIDE (all of the tile's rows
+// exist): the (fm, r) part of the row goes into the scalar offset; otherwise
+// every element gets its own vector offset, which the descriptor checks. Each
+// kind of load is one loop with no branch inside, so a wave's loads are all in
+// flight together.
+template <class Mma, bool INSIDE>
+struct TileIo {
+  static constexpr int FM = Mma::FM;
+  static constexpr int FN = Mma::FN;
+  typedef f32x16_t Acc[FM][FN];
+
+  __device__ __forceinline__ static int rrow(int fm, int r) { return fm * 32 + 8 * (r >> 2) + (r & 3); }
+  __device__ __forceinline__ static uint32_t voff(const uint32_t* coff, int ldc, int fm, int fn,
+                                                  int r, int size) {
+    if (INSIDE) return coff[fn] * (uint32_t)size;
+    return (coff[fn] + (uint32_t)(rrow(fm, r) * ldc)) * (uint32_t)size;
+  }
+  __device__ __forceinline__ static int soff(int ldc, int fm, int r, int size) {
+    return INSIDE ? rrow(fm, r) * ldc * size : 0;
+  }
+  __device__ __forceinline__ static float ld32(__amdgpu_buffer_rsrc_t rs, const uint32_t* coff,
+                                               int ldc, int fm, int fn, int r) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                         rs, voff(coff, ldc, fm, fn, r, 4), soff(ldc, fm, r, 4), 0));
+  }
+  __device__ __forceinline__ static float ld16(__amdgpu_buffer_rsrc_t rs, const uint32_t* coff,
+                                               int ldc, int fm, int fn, int r) {
+    return __uint_as_float((uint32_t)__builtin_amdgcn_raw_buffer_load_b16(
+                               rs, voff(coff, ldc, fm, fn, r, 2), soff(ldc, fm, r, 2), 0)
+                           << 16);
+  }
+
+  // acc = Cpart (if part) + old output (if acc_old; bf16 when out16); blocks
+  // past the output are left as they are (never stored)
+  __device__ __forceinline__ static void init(Acc& acc, __amdgpu_buffer_rsrc_t rc,
+                                              __amdgpu_buffer_rsrc_t rp, const uint32_t* coff,
+                                              const bool* ok, int ldc, bool part, bool acc_old,
+                                              bool out16) {
+    if (part) {
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn)
+        if (ok[fn]) {
+#pragma unroll
+          for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[fm][fn][r] = ld32(rp, coff, ldc, fm, fn, r);
+        }
+      if (acc_old) {  // and the old bf16 output: one column block at a time
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) {
+          if (!ok[fn]) continue;
+          float old[FM][16];
+#pragma unroll
+          for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) old[fm][r] = ld16(rc, coff, ldc, fm, fn, r);
+#pragma unroll
+          for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[fm][fn][r] += old[fm][r];
+        }
+      }
+    } else if (out16) {
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn)
+        if (ok[fn]) {
+#pragma unroll
+          for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[fm][fn][r] = ld16(rc, coff, ldc, fm, fn, r);
+        }
+    } else {
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn)
+        if (ok[fn]) {
+#pragma unroll
+          for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[fm][fn][r] = ld32(rc, coff, ldc, fm, fn, r);
+        }
+    }
+  }
+
+  __device__ __forceinline__ static void store(const Acc& acc, __amdgpu_buffer_rsrc_t rc,
+                                               const uint32_t* coff, const bool* ok, int ldc,
+                                               bool out16) {
+    if (out16) {
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) {
+        if (!ok[fn]) continue;
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            __builtin_amdgcn_raw_buffer_store_b16(to_storage<Bf16>(acc[fm][fn][r]), rc,
+                                                  voff(coff, ldc, fm, fn, r, 2), soff(ldc, fm, r, 2), 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) {
+        if (!ok[fn]) continue;
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[fm][fn][r]), rc,
+                                                  voff(coff, ldc, fm, fn, r, 4), soff(ldc, fm, r, 4), 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  }
+};
+
 template <class Mma>
 __device__ __forceinline__ void wide_tile(const GemmGroup& g, int tm, int tn, int64_t mext,
                                           int64_t next, char* smem, int tid) {
@@ -87,66 +207,49 @@ __device__ __forceinline__ void wide_tile(const GemmGroup& g, int tm, int tn, in
   const int wn = wave / Mma::kWGM;
   const int64_t m0 = (int64_t)tm * Mma::kBM;
   const int64_t n0 = (int64_t)tn * Mma::kBN;
-  Mma mma;
-  mma.run(static_cast<const char*>(g.A), g.lda * 2, m0, g.rows, static_cast<const char*>(g.B),
-          g.ldb * 2, n0, g.cols, g.K * 2, smem, tid);
-  // Epilogue through buffer descriptors over the tile's rows [m0, m0 + BM)
-  // that exist (rows past mext fall outside them: their loads return 0 and
-  // their stores are dropped), so each element's address is a 32-bit offset.
-  // One column block (FM x 32 x 32 values per wave) at a time: every value to
-  // add to it (the old output, or the partial sums of earlier chunks) is loaded
-  // before any is used, so a read-modify-write tile waits for memory FN times
-  // rather than once per 32 x 32 block.
+  // Output through buffer descriptors over the tile's rows [m0, m0 + BM) that
+  // exist (rows past mext fall outside them: their loads return 0 and their
+  // stores are dropped), so each element's address is a 32-bit offset.
   const int64_t rows = mext - m0 < Mma::kBM ? mext - m0 : Mma::kBM;
   const bool out16 = g.Cb != nullptr;
-  const int es = out16 ? 2 : 4;
   const __amdgpu_buffer_rsrc_t rc =
       out16 ? uniform_rsrc(reinterpret_cast<const char*>(g.Cb + m0 * g.ldc), (int)(rows * g.ldc * 2))
             : uniform_rsrc(reinterpret_cast<const char*>(g.C + m0 * g.ldc), (int)(rows * g.ldc * 4));
   const bool part = out16 && g.Cpart;
-  const __amdgpu_buffer_rsrc_t rp =
-      uniform_rsrc(reinterpret_cast<const char*>(part ? g.Cpart + m0 * g.ldc : g.C), part ? (int)(rows * g.ldc * 4) : 0);
+  const __amdgpu_buffer_rsrc_t rp = uniform_rsrc(
+      reinterpret_cast<const char*>(part ? g.Cpart + m0 * g.ldc : g.C), part ? (int)(rows * g.ldc * 4) : 0);
   const bool acc_old = g.accumulate != 0;
   const int ldc = (int)g.ldc;
+
+  uint32_t coff[FN];
+  bool ok[FN];
+  const int wnu = __builtin_amdgcn_readfirstlane(wn);
 #pragma unroll
   for (int fn = 0; fn < FN; ++fn) {
     const int col = (int)n0 + Mma::col_of(wn, fn, lane);
-    const bool colok = col < next;
-    float add[FM][16];
-    if (acc_old || part) {
-#pragma unroll
-      for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int e = Mma::row_of(wm, fm, r, lane) * ldc + col;
-          float v = 0.f;
-          if (colok) {
-            if (part) v = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rp, e * 4, 0, 0));
-            if (acc_old) {
-              if (out16)
-                v += __uint_as_float((uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rc, e * 2, 0, 0) << 16);
-              else
-                v += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rc, e * 4, 0, 0));
-            }
-          }
-          add[fm][r] = v;
-        }
-    }
-#pragma unroll
-    for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int e = Mma::row_of(wm, fm, r, lane) * ldc + col;
-        const float v = mma.acc[fm][fn][r] + ((acc_old || part) ? add[fm][r] : 0.f);
-        if (colok) {
-          if (out16)
-            __builtin_amdgcn_raw_buffer_store_b16(to_storage<Bf16>(v), rc, e * es, 0, 0);
-          else
-            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), rc, e * es, 0, 0);
-        }
-      }
-    __builtin_amdgcn_sched_barrier(0);
+    coff[fn] = (uint32_t)(Mma::row_of(wm, 0, 0, lane) * ldc + col);
+    ok[fn] = n0 + wnu * Mma::WTN + fn * 32 < next;  // the whole 32-column block (wave-uniform)
   }
+  const bool inside = m0 + Mma::kBM <= mext;
+
+  // A read-modify-write output (accumulate, or the fp32 partial sums of
+  // earlier chunks) is read straight into the accumulators before the K loop,
+  // so the product is added to it there and the epilogue only stores; the
+  // reads' latency overlaps the first K-tile's loads.
+  Mma mma;
+  mma.run_from(static_cast<const char*>(g.A), g.lda * 2, m0, g.rows, static_cast<const char*>(g.B),
+               g.ldb * 2, n0, g.cols, g.K * 2, smem, tid, [&]() {
+                 if (!part && !acc_old)
+                   mma.zero();
+                 else if (inside)
+                   TileIo<Mma, true>::init(mma.acc, rc, rp, coff, ok, ldc, part, acc_old, out16);
+                 else
+                   TileIo<Mma, false>::init(mma.acc, rc, rp, coff, ok, ldc, part, acc_old, out16);
+               });
+  if (inside)
+    TileIo<Mma, true>::store(mma.acc, rc, coff, ok, ldc, out16);
+  else
+    TileIo<Mma, false>::store(mma.acc, rc, coff, ok, ldc, out16);
 }
 
 template <class MmaH, class MmaW>
