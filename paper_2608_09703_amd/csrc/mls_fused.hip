@@ -125,12 +125,51 @@ __global__ __launch_bounds__(Mma::NT, MINB) void fused_fwd_kernel(FusedArgs a) {
         }
       mb = fmaxf(mb, shfl_xor32(mb));
 
-      if constexpr (STORE) {
-        // four consecutive vocabulary rows of one token per 8-byte store; the
-        // two lane halves fill 16 contiguous bytes, a wave's 64 rows one
-        // 128-byte line per token (staging through LDS for whole-line stores
-        // needs 16 KB more per block, which costs the second block per CU:
-        // slower)
+      if constexpr (STORE && TAU1) {
+        // The wave's 64 rows x 32 tokens go through its own 4 KB of LDS, token
+        // by token (16-byte chunks XOR-swizzled with the token), and leave as
+        // whole 128-byte lines of token-major slab rows: eight lines per store
+        // instruction instead of 32 partial ones. The staging area is the
+        // second pipeline stage, which is idle here: the product just ended
+        // with a barrier after every wave's last read, and the next product
+        // fills only the first stage before its first barrier, which no wave
+        // passes before every wave's staging reads are done (stage_barrier
+        // drains them). Only this wave touches its area and its LDS accesses
+        // complete in order, so no barrier is needed here.
+        static_assert(Mma::kStageBytes >= Mma::NW * 32 * 128 && Mma::WTM == 64, "staging fits");
+        char* stg = smem + Mma::kStageBytes + wave * 32 * 128;
+        const int c = lane & 31;  // token inside the 32-token block
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+          for (int rg = 0; rg < 4; ++rg) {
+            uint32_t w[2];
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+              const float x0 = mma.acc[fm][fn][rg * 4 + 2 * k] - mb;
+              const float x1 = mma.acc[fm][fn][rg * 4 + 2 * k + 1] - mb;
+              w[k] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)x0) |
+                     ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)x1) << 16);
+            }
+            const int chunk = (fm * 4 + rg) ^ (c & 7);  // 8 vocabulary rows per chunk
+            *reinterpret_cast<uint2*>(stg + c * 128 + chunk * 16 + hi * 8) = make_uint2(w[0], w[1]);
+          }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        uint16_t* rows = a.lslab + ((int64_t)i * a.n_tt * BN + tbase + wn * Mma::WTN + fn * 32) *
+                                       a.ld_lslab + vbase + wm * Mma::WTM;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int tr = q * 8 + (lane >> 3);
+          const int kk = lane & 7;
+          const uint4 v = *reinterpret_cast<const uint4*>(stg + tr * 128 + ((kk ^ (tr & 7)) << 4));
+          *reinterpret_cast<uint4*>(rows + (int64_t)tr * a.ld_lslab + kk * 8) = v;
+        }
+      }
+      if constexpr (STORE && !TAU1) {
+        // At tau != 1 the staging's registers cost spills (the teacher's fp32
+        // weights are live), so four consecutive vocabulary rows of one token
+        // go out per 8-byte store instead: the two lane halves fill 16
+        // contiguous bytes, a wave's 64 rows one 128-byte line per token.
         const int c = Mma::col_of(wn, fn, lane);
         uint16_t* row = a.lslab + ((int64_t)i * a.n_tt * BN + tbase + c) * a.ld_lslab + vbase;
 #pragma unroll
