@@ -237,8 +237,10 @@ mls_status mls_distill_fwd_bwd(const mls_problem* p, void* stats, float* ce, flo
  * NULL) receives every token's top-1 index per sub-model. One pass over the
  * logits, normalised as it goes: no forward statistics are needed (tau and
  * teacher do not matter here). The workspace of mls_query_sizes suffices.
- * M must be at most 4 (MLS_UNSUPPORTED otherwise). With no valid token the
- * outputs are 0. Asynchronous on stream.
+ * A pass holds at most 4 sub-models; a larger suite runs one pass per subset
+ * of 4, the subsets chosen so that every pair of sub-models shares one (e.g.
+ * 6 passes for M = 8), each staged in the workspace and scattered into the
+ * outputs. With no valid token the outputs are 0. Asynchronous on stream.
  */
 mls_status mls_diagnostics(const mls_problem* p, float* kl_pair, float* agree, int32_t* argmax,
                            void* workspace, size_t workspace_bytes, void* stream);

@@ -125,7 +125,8 @@ struct Plan {
   size_t off_slab = 0, off_slabT = 0, off_hT = 0, off_WT = 0, off_ghp = 0, bwd_bytes = 0;
   // diagnostics workspace (vocabulary segments of the pairwise pass)
   int n_vt_diag = 0, n_tt_diag = 0;
-  size_t off_dpart = 0, off_drow = 0, diag_bytes = 0;
+  int m_diag = 0;  // sub-models per diagnostics pass (at most kMaxDiagModels)
+  size_t off_dpart = 0, off_drow = 0, off_dsub = 0, off_dam = 0, diag_bytes = 0;
   size_t ws_bytes = 0;
   size_t stats_bytes = 0;
   size_t header_off = 0;
@@ -234,16 +235,26 @@ void make_plan(const mls_problem* p, Plan& pl) {
   }
   pl.bwd_bytes = off;
 
-  // diagnostics: one record per (vocabulary tile, token)
-  if (pl.M <= kMaxDiagModels) {
+  // diagnostics: one record per (vocabulary tile, token) of the sub-models of
+  // one pass; suites of more than kMaxDiagModels run several passes over
+  // subsets, each staged and scattered into the outputs
+  {
+    const int md = std::min(pl.M, kMaxDiagModels);
+    pl.m_diag = md;
     pl.n_vt_diag = (int)((p->V + diag_tile_rows(pl.wide) - 1) / diag_tile_rows(pl.wide));
-    pl.n_tt_diag = (int)((p->T + diag_tile_cols(pl.wide, pl.M) - 1) / diag_tile_cols(pl.wide, pl.M));
+    pl.n_tt_diag = (int)((p->T + diag_tile_cols(pl.wide, md) - 1) / diag_tile_cols(pl.wide, md));
     off = 0;
     pl.off_dpart = off;
-    off = align256(off + (size_t)pl.n_vt_diag * kDiagParts * pl.T * diag_record_floats(pl.M) *
+    off = align256(off + (size_t)pl.n_vt_diag * kDiagParts * pl.T * diag_record_floats(md) *
                              sizeof(float));
     pl.off_drow = off;
-    off = align256(off + (size_t)pl.T * 2 * pl.M * pl.M * sizeof(float));
+    off = align256(off + (size_t)pl.T * 2 * md * md * sizeof(float));
+    if (pl.M > kMaxDiagModels) {
+      pl.off_dsub = off;
+      off = align256(off + 2 * kMaxDiagModels * kMaxDiagModels * sizeof(float));
+      pl.off_dam = off;
+      off = align256(off + (size_t)kMaxDiagModels * pl.T * sizeof(int32_t));
+    }
     pl.diag_bytes = off;
   }
   pl.ws_bytes = std::max(std::max(pl.fwd_bytes, pl.bwd_bytes), pl.diag_bytes);
@@ -910,8 +921,6 @@ mls_status mls_diagnostics(const mls_problem* p, float* kl_pair, float* agree, i
   g_last_error.clear();
   mls_status st = validate(p);
   if (st != MLS_OK) return st;
-  if (p->M > kMaxDiagModels)
-    return fail(MLS_UNSUPPORTED, "diagnostics support M <= %d, got %d", kMaxDiagModels, p->M);
   if (!kl_pair || !agree || !workspace)
     return fail(MLS_INVALID_ARG, "kl_pair, agree and workspace must be non-NULL");
   if (!aligned(workspace, 16) || !aligned(kl_pair, 4) || !aligned(agree, 4) || !aligned(argmax, 4))
@@ -922,13 +931,48 @@ mls_status mls_diagnostics(const mls_problem* p, float* kl_pair, float* agree, i
     return fail(MLS_WORKSPACE_TOO_SMALL, "diagnostics need %zu workspace bytes, got %zu",
                 pl.diag_bytes, workspace_bytes);
   char* ws = static_cast<char*>(workspace);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // Passes: the whole suite, or subsets of kMaxDiagModels sub-models chosen
+  // greedily (each adds the most pairs not yet covered) until every pair of
+  // sub-models has shared a pass (a pair's KL and agreement need both logits).
+  int subsets[64][kMaxDiagModels];
+  int n_pass = 0;
+  if (pl.M <= kMaxDiagModels) {
+    for (int i = 0; i < pl.M; ++i) subsets[0][i] = i;
+    n_pass = 1;
+  } else {
+    bool covered[kMaxModels][kMaxModels] = {};
+    for (;;) {
+      int best[kMaxDiagModels] = {0, 1, 2, 3}, best_gain = 0;
+      int c[kMaxDiagModels];
+      for (c[0] = 0; c[0] < pl.M; ++c[0])
+        for (c[1] = c[0] + 1; c[1] < pl.M; ++c[1])
+          for (c[2] = c[1] + 1; c[2] < pl.M; ++c[2])
+            for (c[3] = c[2] + 1; c[3] < pl.M; ++c[3]) {
+              int gain = 0;
+              for (int x = 0; x < kMaxDiagModels; ++x)
+                for (int y = x + 1; y < kMaxDiagModels; ++y) gain += covered[c[x]][c[y]] ? 0 : 1;
+              if (gain > best_gain) {
+                best_gain = gain;
+                memcpy(best, c, sizeof(best));
+              }
+            }
+      if (best_gain == 0) break;
+      memcpy(subsets[n_pass++], best, sizeof(best));
+      for (int x = 0; x < kMaxDiagModels; ++x)
+        for (int y = 0; y < kMaxDiagModels; ++y) covered[best[x]][best[y]] = true;
+    }
+  }
+  for (int ps_i = 0; ps_i < n_pass; ++ps_i) {
+  const int* sub = subsets[ps_i];
+  const bool staged = pl.M > kMaxDiagModels;
   DiagArgs a;
   memset(&a, 0, sizeof(a));
-  a.M = pl.M;
-  for (int i = 0; i < pl.M; ++i) {
-    a.h[i] = p->h[i];
-    a.W[i] = p->W[i];
-    a.d[i] = p->d[i];
+  a.M = pl.m_diag;
+  for (int k = 0; k < pl.m_diag; ++k) {
+    a.h[k] = p->h[sub[k]];
+    a.W[k] = p->W[sub[k]];
+    a.d[k] = p->d[sub[k]];
   }
   a.T = p->T;
   a.V = p->V;
@@ -939,10 +983,11 @@ mls_status mls_diagnostics(const mls_problem* p, float* kl_pair, float* agree, i
   a.group_v = 4;  // measured: 4 > 8 > 16 here (8 for the forward and backward)
   a.partials = reinterpret_cast<float*>(ws + pl.off_dpart);
   a.rowvals = reinterpret_cast<float*>(ws + pl.off_drow);
-  a.kl_pair = kl_pair;
-  a.agree = agree;
-  a.argmax = argmax;
-  hipStream_t s = static_cast<hipStream_t>(stream);
+  float* sub_out = reinterpret_cast<float*>(ws + pl.off_dsub);
+  int32_t* am_sub = reinterpret_cast<int32_t*>(ws + pl.off_dam);
+  a.kl_pair = staged ? sub_out : kl_pair;
+  a.agree = staged ? sub_out + kMaxDiagModels * kMaxDiagModels : agree;
+  a.argmax = staged ? (argmax ? am_sub : nullptr) : argmax;
   hipError_t e;
   {
     ProfScope ps("diag_tiles", s);
@@ -954,6 +999,26 @@ mls_status mls_diagnostics(const mls_problem* p, float* kl_pair, float* agree, i
     e = launch_diag_reduce(a, s);
   }
   if (e != hipSuccess) return hip_fail(e, "diagnostics reduction launch");
+  if (staged) {
+    DiagScatterArgs sc;
+    memset(&sc, 0, sizeof(sc));
+    sc.M = pl.M;
+    sc.n = pl.m_diag;
+    for (int k = 0; k < pl.m_diag; ++k) sc.sub[k] = sub[k];
+    sc.T = p->T;
+    sc.kl_sub = a.kl_pair;
+    sc.agree_sub = a.agree;
+    sc.am_sub = a.argmax;
+    sc.kl_pair = kl_pair;
+    sc.agree = agree;
+    sc.argmax = argmax;
+    {
+      ProfScope ps("diag_scatter", s);
+      e = launch_diag_scatter(sc, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "diagnostics scatter launch");
+  }
+  }
   return MLS_OK;
 }
 

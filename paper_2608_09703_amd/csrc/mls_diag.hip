@@ -5,7 +5,9 @@
 //
 // One pass, normalising itself. One block owns one (vocabulary tile, token
 // tile) pair, as the fused forward does, and computes the logits tile of every
-// sub-model (all M accumulator sets stay in registers, M <= 4). Per token and
+// sub-model (all M accumulator sets stay in registers, M <= 4; larger suites
+// run one such pass per subset of four sub-models, the subsets covering every
+// pair). Per token and
 // sub-model i, relative to the largest logit m_i seen so far:
 //   Z_i  = sum_v exp(l_i - m_i)
 //   S_ij = sum_v exp(l_i - m_i) (l_i - l_j)      for every ordered pair i != j
@@ -333,7 +335,27 @@ hipError_t launch_reduce_m(const DiagArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+__global__ __launch_bounds__(kThreads) void diag_scatter_kernel(DiagScatterArgs a) {
+  const int64_t t = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (t < (int64_t)a.n * a.n) {
+    const int r = (int)t / a.n;
+    const int c = (int)t % a.n;
+    a.kl_pair[a.sub[r] * a.M + a.sub[c]] = a.kl_sub[t];
+    a.agree[a.sub[r] * a.M + a.sub[c]] = a.agree_sub[t];
+  }
+  if (a.argmax && t < a.T) {
+    for (int k = 0; k < a.n; ++k) a.argmax[(int64_t)a.sub[k] * a.T + t] = a.am_sub[(int64_t)k * a.T + t];
+  }
+}
+
 }  // namespace
+
+hipError_t launch_diag_scatter(const DiagScatterArgs& a, hipStream_t stream) {
+  const int64_t n = a.T > 64 ? a.T : 64;
+  hipLaunchKernelGGL(diag_scatter_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads),
+                     0, stream, a);
+  return hipGetLastError();
+}
 
 int diag_tile_rows(bool wide) { return wide ? kFusedWideBM : kFusedBM; }
 int diag_tile_cols(bool wide, int M) { return wide ? (M == 4 ? kDiagBN / 2 : kDiagBN) : kDiagGenBN; }

@@ -201,6 +201,22 @@ struct DiagArgs {
   int32_t* argmax;        // [M][T] or null
 };
 
+// Scatter of one diagnostics pass over a subset of at most kMaxDiagModels
+// sub-models (sub[k] is the sub-model of slot k) into the [M][M] outputs and
+// the [M][T] argmax rows.
+struct DiagScatterArgs {
+  int32_t M;
+  int32_t n;  // slots used
+  int32_t sub[kMaxDiagModels];
+  int64_t T;
+  const float* kl_sub;     // [n][n]
+  const float* agree_sub;  // [n][n]
+  const int32_t* am_sub;   // [n][T] or null
+  float* kl_pair;          // [M][M]
+  float* agree;            // [M][M]
+  int32_t* argmax;         // [M][T] or null
+};
+
 // Inter-model junction (eq. (1)).
 struct JunctionArgs {
   int64_t T;
@@ -296,6 +312,7 @@ int diag_tile_cols(bool wide, int M);
 int diag_record_floats(int M);
 hipError_t launch_diag_tiles(const DiagArgs& a, bool f32, bool wide, hipStream_t stream);
 hipError_t launch_diag_reduce(const DiagArgs& a, hipStream_t stream);
+hipError_t launch_diag_scatter(const DiagScatterArgs& a, hipStream_t stream);
 bool junction_shape(int64_t width, int* tpr, int* cpl);
 int64_t junction_max_width();
 hipError_t launch_junction_fwd(const JunctionArgs& a, bool act_f32, hipStream_t stream);

@@ -234,11 +234,10 @@ def test_chunk_width_is_rounded():
 def test_diagnostics_reject_bad_arguments_before_device_work():
     fake = 1 << 40
     out = fake + (1 << 30)
-    p = _fake_problem(M=5)
-    ws, _ = B.query_sizes(p)
-    with pytest.raises(B.MlsError) as e:  # more sub-models than the pairwise pass holds
-        B.diagnostics(p, out, out + 256, None, fake + (1 << 20), ws, None)
-    assert e.value.status == B.MLS_UNSUPPORTED
+    p = _fake_problem(M=8)  # accepted (passes over subsets), checked like any other call
+    with pytest.raises(B.MlsError) as e:
+        B.diagnostics(p, out, out + 256, None, fake + (1 << 20), 1024, None)
+    assert e.value.status == B.MLS_WORKSPACE_TOO_SMALL
     p = _fake_problem()
     ws, _ = B.query_sizes(p)
     with pytest.raises(B.MlsError) as e:

@@ -110,6 +110,15 @@ SMALL = [
                                   ignore_frac=0.1, seed=30), True),
     ("m4_large_logits", WL.custom(4, 150, (64, 64, 128, 256), 1100, w_std=None, w_scale=20.0,
                                   seed=36), False),
+    # more than four sub-models: passes over subsets of four that cover every pair
+    ("m5_nested_subsets", WL.custom(5, 220, (64, 64, 128, 128, 192), 900, w_std=0.1, w_scale=3.0,
+                                    ignore_frac=0.1, seed=37), True),
+    ("m8_nested_subsets", WL.custom(8, 200, (64, 64, 128, 128, 192, 192, 256, 320), 1100,
+                                    w_std=0.1, w_scale=3.0, ignore_frac=0.1, seed=38), True),
+    ("m6_general_bf16", WL.custom(6, 140, (40, 72, 72, 136, 136, 200), 650, w_std=0.1, w_scale=2.0,
+                                  seed=39), True),
+    ("m7_f32", WL.custom(7, 130, (32, 36, 36, 64, 64, 100, 100), 555, dtype="f32", w_std=0.1,
+                         w_scale=2.0, ignore_frac=0.1, seed=40), False),
 ]
 
 
