@@ -13,7 +13,9 @@ import os
 from typing import Optional, Sequence
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libmls.so")
+# MLS_LIBRARY selects another build of the same library (e.g. the host-sanitized
+# copy for CPU-only host tests); by default the in-tree libmls.so.
+LIB_PATH = os.environ.get("MLS_LIBRARY") or os.path.join(PKG, "libmls.so")
 
 MAX_MODELS = 8
 
