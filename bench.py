@@ -154,6 +154,9 @@ def parse():
                     help="time the inter-model junctions (forward + backward) instead")
     ap.add_argument("--decode", action="store_true",
                     help="time the speculative-decoding head step instead")
+    ap.add_argument("--mfma-ceiling", action="store_true",
+                    help="measure the device's bf16 MFMA ceiling (register operands, zero and random "
+                         "data) instead")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB (a known-size "
                          "kernel to calibrate HBM byte counters)")
@@ -553,6 +556,47 @@ def main_decode(args):
     print(json.dumps(out), flush=True)
 
 
+def main_mfma_ceiling(args):
+    """Rate of independent v_mfma_f32_32x32x16_bf16 on register operands (no memory,
+    no LDS) with all-zero and with random bf16 operands: the ceiling any kernel built
+    on this instruction can reach on this device, next to the nominal peak."""
+    import torch
+    from paper_2608_09703_amd import binding as B
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    sink = torch.empty(B.MFMA_PROBE_SINK_FLOATS, dtype=torch.float32, device=dev)
+    iters = 20000
+    res = {}
+    for kind in ("zero", "random"):
+        flops = B.mfma_probe(kind == "random", iters, None, 0, None)
+        fn = lambda: B.mfma_probe(kind == "random", iters, sink.data_ptr(), sink.numel(),  # noqa: E731
+                                  stream.cuda_stream)
+        for _ in range(args.warmup):
+            fn()
+        st = step_stats(time_steps(torch, fn, stream, args.steps))
+        res[kind] = {"ms_per_launch": st["median"], "tflops": flops / (st["median"] / 1e3) / 1e12,
+                     "frac_of_nominal": flops / (st["median"] / 1e3) / PEAK_FLOPS["bf16"]}
+        log(f"{kind:6s} operands: {res[kind]['tflops']:.0f} TFLOP/s "
+            f"({100 * res[kind]['frac_of_nominal']:.1f}% of the nominal bf16 peak)")
+    device = device_peaks()
+    out = {
+        "metric": "bf16 MFMA ceiling, v_mfma_f32_32x32x16_bf16 on register operands (TFLOP/s)",
+        "value": res["random"]["tflops"], "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": res["random"]["ms_per_launch"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic register operands (zero, and random bf16 in +-[1, 2))",
+        "config": {"workload": "mfma_ceiling", "blocks": 2048, "threads": 256,
+                   "chains_per_wave": 8, "iters": iters, "parallelism": "single GPU"},
+        "zero_operands": res["zero"], "random_operands": res["random"], "device": device,
+        "roofline": {"bound": "mfma", "kernel": "mfma_probe", "achieved": res["random"]["tflops"],
+                     "peak": PEAK_FLOPS["bf16"] / 1e12, "unit": "TFLOP/s",
+                     "frac": res["random"]["frac_of_nominal"], "traffic": 0},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -565,6 +609,8 @@ def main():
         return main_junction(args)
     if args.decode:
         return main_decode(args)
+    if args.mfma_ceiling:
+        return main_mfma_ceiling(args)
 
     import torch
     from paper_2608_09703_amd import binding as B

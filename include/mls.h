@@ -440,6 +440,19 @@ typedef struct mls_kernel_time {
 mls_status mls_profile_enable(int32_t enable);
 mls_status mls_profile_report(mls_kernel_time* out, int32_t max_entries, int32_t* n_out);
 
+/*
+ * Measurement aid: the MFMA ceiling of the device. Enqueues one launch in which
+ * every wave issues iters x 8 independent v_mfma_f32_32x32x16_bf16 on operands
+ * held in registers (no memory or LDS traffic): all-zero operands, or random
+ * bf16 values when random_operands is nonzero (the clock responds to the data's
+ * switching activity). *flops receives the launch's floating-point operations
+ * (divide by its duration for the rate). sink: device float32 array of at least
+ * 524288 entries that receives per-thread sums (it keeps the work live); with
+ * sink NULL only *flops is written. Asynchronous on stream.
+ */
+mls_status mls_mfma_probe(int32_t random_operands, int32_t iters, float* sink, size_t sink_floats,
+                          double* flops, void* stream);
+
 /* Static text for a status code. */
 const char* mls_status_string(mls_status s);
 

@@ -65,6 +65,7 @@ EXPORTED = (
     "mls_device_info",
     "mls_profile_enable",
     "mls_profile_report",
+    "mls_mfma_probe",
 )
 
 
@@ -169,6 +170,8 @@ def lib():
         L.mls_version.restype = ctypes.c_char_p
         ip = ctypes.POINTER(ctypes.c_int32)
         L.mls_device_info.argtypes = [ip, ip, ip, ip]
+        L.mls_mfma_probe.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, ctypes.c_size_t,
+                                     ctypes.POINTER(ctypes.c_double), vp]
         L.mls_profile_enable.argtypes = [ctypes.c_int32]
         L.mls_profile_report.argtypes = [ctypes.POINTER(KernelTime), ctypes.c_int32,
                                          ctypes.POINTER(ctypes.c_int32)]
@@ -351,6 +354,18 @@ def device_error(p: Problem, stats: int, stream: int) -> int:
     """OR of the MLS_DEVFLAG_* bits the last forward on ``stats`` raised (waits for the stream)."""
     f = ctypes.c_int32(0)
     check(lib().mls_device_error(ctypes.byref(p), stats, stream, ctypes.byref(f)), "mls_device_error")
+    return f.value
+
+
+MFMA_PROBE_SINK_FLOATS = 524288
+
+
+def mfma_probe(random_operands: bool, iters: int, sink: Optional[int], sink_floats: int,
+               stream: Optional[int]) -> float:
+    """Enqueues the MFMA ceiling probe (or, with sink None, only sizes it); returns its FLOPs."""
+    f = ctypes.c_double(0.0)
+    check(lib().mls_mfma_probe(1 if random_operands else 0, iters, sink, sink_floats,
+                               ctypes.byref(f), stream), "mls_mfma_probe")
     return f.value
 
 

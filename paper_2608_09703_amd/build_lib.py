@@ -19,7 +19,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libmls.so")
 
-SOURCES = ["mls_api.cpp", "mls_fused.hip", "mls_gemm.hip", "mls_rows.hip", "mls_diag.hip", "mls_junction.hip", "mls_decode.hip", "mls_static.hip"]
+SOURCES = ["mls_api.cpp", "mls_fused.hip", "mls_gemm.hip", "mls_rows.hip", "mls_diag.hip", "mls_junction.hip", "mls_decode.hip", "mls_static.hip",
+           "mls_probe.hip"]
 ARCH = "gfx950"
 
 

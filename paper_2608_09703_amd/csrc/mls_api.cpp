@@ -1327,6 +1327,25 @@ mls_status mls_device_error(const mls_problem* p, const void* stats, void* strea
   return mls_read_stats_header(p, stats, stream, nullptr, flags);
 }
 
+mls_status mls_mfma_probe(int32_t random_operands, int32_t iters, float* sink, size_t sink_floats,
+                          double* flops, void* stream) {
+  g_last_error.clear();
+  if (iters < 1 || iters > (1 << 24)) return fail(MLS_INVALID_ARG, "iters=%d out of range", iters);
+  if (!flops) return fail(MLS_INVALID_ARG, "flops is NULL");
+  *flops = mfma_probe_flops(iters);
+  if (!sink) return MLS_OK;  // size query
+  if (sink_floats < (size_t)mfma_probe_sink_floats() || !aligned(sink, 4))
+    return fail(MLS_INVALID_ARG, "sink needs %lld floats", (long long)mfma_probe_sink_floats());
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  {
+    ProfScope ps("mfma_probe", s);
+    e = launch_mfma_probe(random_operands ? 1 : 0, iters, sink, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "probe launch");
+  return MLS_OK;
+}
+
 mls_status mls_profile_enable(int32_t enable) {
   g_last_error.clear();
   g_prof.on = enable != 0;

@@ -291,6 +291,11 @@ struct VerifyArgs {
   int32_t* next_token;         // [batch]
 };
 
+// MFMA ceiling probe (measurement aid).
+hipError_t launch_mfma_probe(int random, int iters, float* sink, hipStream_t stream);
+double mfma_probe_flops(int iters);
+int64_t mfma_probe_sink_floats();
+
 // Sets the calling thread's mls_last_error text to "what: detail" and returns s.
 mls_status set_error(mls_status s, const char* what, const char* detail);
 
