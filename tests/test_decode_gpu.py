@@ -7,9 +7,11 @@
   inverse-CDF position, acceptance) from fp32 arithmetic on the GPU and fp64 in
   the oracle, on the same fp32 logits. A GPU result that differs from the
   oracle's is accepted only when the oracle reproduces it under a perturbation
-  of 1e-5 of its inputs (the uniform, top_p, or the acceptance ratio), and such
-  rows must stay rare. Greedy decisions are taken on identical fp32 values and
-  must match exactly.
+  of 1e-5 of its inputs (the uniform, top_p, or the acceptance ratio; for
+  sampled tokens also with probabilities within 2^-20 of the nucleus boundary
+  taken in either order, which fp32 weights cannot rank), and such rows must
+  stay rare: each test states how many it allows and prints how many it saw.
+  Greedy decisions are taken on identical fp32 values and must match exactly.
 """
 
 import numpy as np
@@ -18,12 +20,12 @@ import torch
 
 from oracle import decode as OD
 from paper_2608_09703_amd import api as D
+from tests.decode_checks import EPS, FLAT_ROWS_ALLOWED, check_samples as _check_samples
 from paper_2608_09703_amd import workloads as WL
 
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda:0"
-EPS = 1e-5
 
 
 def _np(x):
@@ -63,28 +65,6 @@ def test_head_logits(case):
 # ---------------------------------------------------------------------------
 # sampling
 # ---------------------------------------------------------------------------
-
-def _oracle_tokens_near(row, u, temperature, top_p):
-    """Tokens the oracle draws under perturbations of u and top_p by EPS."""
-    out = set()
-    for du in (-EPS, 0.0, EPS):
-        for dp in (-EPS, 0.0, EPS):
-            uu = min(max(u + du, 0.0), 1.0 - 1e-12)
-            pp = min(max(top_p + dp, 1e-9), 1.0)
-            out.add(int(OD.draw(OD.filtered_probs(row, temperature, pp), uu)))
-    return out
-
-
-def _check_samples(logits, u, tokens, temperature, top_p, max_ambiguous=0.02):
-    ref = OD.sample(logits, u, temperature, top_p)
-    miss = np.nonzero(ref != tokens)[0]
-    for r in miss:
-        near = _oracle_tokens_near(logits[r], float(u[r]), temperature, top_p)
-        assert int(tokens[r]) in near, (f"row {r}: GPU token {tokens[r]}, oracle {ref[r]}, "
-                                        f"oracle under perturbation {sorted(near)}")
-    assert len(miss) <= max(1, max_ambiguous * len(tokens)), f"{len(miss)} ambiguous rows"
-    return len(miss)
-
 
 SAMPLE = [
     # rows, V, temperature, top_p, logit scale
@@ -129,7 +109,7 @@ def test_sample_across_logit_scales(scale, top_p):
     u = torch.rand(rows, generator=g, device=DEV)
     tok = _np(D.sample(logits, u, temperature=1.0, top_p=top_p)).astype(np.int64)
     _check_samples(_np(logits).astype(np.float64), _np(u).astype(np.float64), tok, 1.0, top_p,
-                   max_ambiguous=0.05)
+                   allowed=FLAT_ROWS_ALLOWED if scale < 0.1 else 0)
 
 
 def test_sample_ties_and_extreme_uniforms():
@@ -216,11 +196,12 @@ def test_verify_parity(B, G, V, temp, top_p):
                                  temperature=temp, top_p=top_p)
     n_gpu, x_gpu = _np(n_gpu).astype(np.int64), _np(x_gpu).astype(np.int64)
     miss = np.nonzero((n_gpu != n_ref) | (x_gpu != x_ref))[0]
+    print(f"[decode] verified sequences differing from the oracle: {len(miss)} of {B}", flush=True)
     for b in miss:
         outs, base = _ambiguous_sequence(dln, tln, drafts, ua, us, temp, top_p, b)
         assert (n_gpu[b], x_gpu[b]) in outs, (f"sequence {b}: GPU {(n_gpu[b], x_gpu[b])}, oracle "
                                               f"{base}, under perturbation {sorted(outs)}")
-    assert len(miss) <= max(1, 0.05 * B), f"{len(miss)} ambiguous sequences"
+    assert len(miss) == 0, f"{len(miss)} ambiguous sequences (none seen on these cases)"
     if G > 0:
         assert 0 < n_ref.sum() < B * G or B < 4  # the case exercises both outcomes
 
@@ -298,10 +279,11 @@ def test_full_size_step():
     n_ref, x_ref = OD.verify(dln, tln, drafts, ua, us, wl.temperature, wl.top_p)
     n_gpu, x_gpu = _np(n_gpu), _np(x_gpu)
     miss = np.nonzero((n_gpu != n_ref) | (x_gpu != x_ref))[0]
+    print(f"[decode] verified sequences differing from the oracle: {len(miss)} of {B}", flush=True)
     for b in miss:
         outs, base = _ambiguous_sequence(dln, tln, drafts, ua, us, wl.temperature, wl.top_p, b)
         assert (n_gpu[b], x_gpu[b]) in outs, (b, (n_gpu[b], x_gpu[b]), base)
-    assert len(miss) <= max(1, 0.05 * B)
+    assert len(miss) == 0, f"{len(miss)} ambiguous sequences (none seen at this size)"
     print(f"[decode] mean accepted {n_ref.mean():.2f} of {G}", flush=True)
 
 
