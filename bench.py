@@ -55,9 +55,9 @@ def sources_sha256():
 
 
 def profiled_traffic(workload, kernel, kind=False):
-    """Per-launch HBM bytes of `kernel` from the committed rocprofv3 counter summary
-    (FETCH_SIZE + WRITE_SIZE scaled by a plain-copy calibration), or None when the
-    summary is missing or the kernel sources changed since it was taken."""
+    """Per-launch bytes beyond L2 of `kernel` (reads + writes, from the TCC_EA0 request
+    counters) in the committed rocprofv3 summary, or None when the summary is missing
+    or the kernel sources changed since it was taken."""
     import re
     kind = {False: "kernels", True: "diagnostics"}.get(kind, kind)
     path = os.path.join(ROOT, "profiles", f"{workload}_{kind}.md")
@@ -159,7 +159,7 @@ def parse():
                          "data) instead")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB (a known-size "
-                         "kernel to calibrate HBM byte counters)")
+                         "kernel that checks the traffic counters of a profile run)")
     return ap.parse_args()
 
 
