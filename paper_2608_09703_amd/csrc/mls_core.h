@@ -136,11 +136,11 @@ __device__ __forceinline__ uint2 lds_read_tr8(const char* p) {
   return __builtin_bit_cast(uint2, v);
 }
 
-// SPREAD: the next K-tile's loads are issued a few at a time across the K-steps
-// of the current one instead of in one burst after the barrier, so their LDS
-// writes interleave with the fragment reads. It pays where a K-tile lasts long
-// enough to cover the load latency from its last K-step (the 256 x 256 GEMM
-// tile), and costs where it does not (the 128 x 128 fused tiles).
+// SPREAD: the next K-tile's loads are issued a few at a time over the first two
+// K-steps of the current one instead of in one burst after the barrier, so their
+// LDS writes interleave with the fragment reads while the last of them still
+// has half a K-tile of lead. It pays where a K-tile lasts long (the 256 x 256
+// GEMM tile), and costs where it does not (the 128 x 128 fused tiles).
 template <int BM, int BN, int WGM, int WGN, int STAGES, int RB = 128, int ALAY = kLayoutKC,
           int BLAY = kLayoutKC, bool SPREAD = false>
 struct WideMma {
@@ -423,7 +423,12 @@ struct WideMma {
         const bool more = nt < nk;
         compute_stage(stage, stage + BM * RB, lane, wm, wn, [&](int kk) {
           if (!more) return;
-          constexpr int kPerStep = (kLoadsPerTile + KSTEPS - 1) / KSTEPS;
+          // the tile's loads in the first two K-steps (on the 256 x 256 GEMM tile:
+          // the A panel's four, then the B panel's four): spread enough that their
+          // LDS writes do not land in one burst, early enough that the last ones
+          // still have half a K-tile to arrive before the next barrier
+          constexpr int kSpreadSteps = KSTEPS < 2 ? KSTEPS : 2;
+          constexpr int kPerStep = (kLoadsPerTile + kSpreadSteps - 1) / kSpreadSteps;
 #pragma unroll
           for (int q = 0; q < kPerStep; ++q) {
             const int j = kk * kPerStep + q;
