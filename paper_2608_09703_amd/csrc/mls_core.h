@@ -423,16 +423,18 @@ struct WideMma {
         const bool more = nt < nk;
         compute_stage(stage, stage + BM * RB, lane, wm, wn, [&](int kk) {
           if (!more) return;
-          // the tile's loads in the first two K-steps (on the 256 x 256 GEMM tile:
-          // the A panel's four, then the B panel's four): spread enough that their
-          // LDS writes do not land in one burst, early enough that the last ones
-          // still have half a K-tile to arrive before the next barrier
+          // the tile's loads in the first two K-steps, the B panel's first (on the
+          // 256 x 256 GEMM tile: B's four, then A's four; B, the head or the
+          // hidden states, is re-read from L2 less often than the slab, so its
+          // loads take longer): spread enough that their LDS writes do not land
+          // in one burst, early enough that the last ones still have half a
+          // K-tile to arrive before the next barrier
           constexpr int kSpreadSteps = KSTEPS < 2 ? KSTEPS : 2;
           constexpr int kPerStep = (kLoadsPerTile + kSpreadSteps - 1) / kSpreadSteps;
 #pragma unroll
           for (int q = 0; q < kPerStep; ++q) {
             const int j = kk * kPerStep + q;
-            if (j < kLoadsPerTile) issue_one(j, ra, rb, offa, offb, ka, kb, st, wave);
+            if (j < kLoadsPerTile) issue_one((j + LA) % kLoadsPerTile, ra, rb, offa, offb, ka, kb, st, wave);
           }
         });
       }
