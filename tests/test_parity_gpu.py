@@ -216,6 +216,18 @@ def test_full_size_sampled_rows(name):
     ghr = oracle.grad_h_rows(hn, Wn, yn, rows[:32], g_ce, g_kl, tau=wl.tau)
     for i in range(wl.M):
         assert_grad_rows(gpu["grad_h"][i][rows[:32]], ghr[i], f"{name} grad_h[{i}] rows")
+    if name == "c2_m3_v50k":
+        # sampled vocabulary rows of grad_W (every token's softmax in fp64: the
+        # forward's cost, about a minute on the host here): some are labels,
+        # most are not
+        valid_labels = np.unique(yn[yn != -100])
+        vrows = np.unique(np.concatenate([rng.choice(wl.V, size=20, replace=False),
+                                          rng.choice(valid_labels, size=4, replace=False)]))
+        gwr = oracle.grad_W_rows(hn, Wn, yn, vrows, g_ce, g_kl, tau=wl.tau)
+        soft = non_label_rows(wl.V, yn)[vrows]
+        for i in range(wl.M):
+            assert_grad_rows(gpu["grad_W"][i][vrows], gwr[i], f"{name} grad_W[{i}] rows",
+                             softmax_rows=soft)
         # every row of the logit gradient sums to zero: sum_v grad_W = 0
         colsum = gpu["grad_W"][i].astype(np.float64).sum(axis=0)
         scale = np.abs(gpu["grad_W"][i]).astype(np.float64).sum(axis=0).max()
