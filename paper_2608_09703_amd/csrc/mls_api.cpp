@@ -397,7 +397,7 @@ hipError_t forward_chunk(const mls_problem* p, const Plan& pl, int64_t t0, int64
   // 8 at 16 token tiles (C2 chunks; 4 and 16 are 5 % slower), 4 at 32 token
   // tiles over 1002 vocabulary tiles (C3 chunks, 5 % faster than 8) and at 64
   // (C4 chunks, 1 %), level at 52 over 2048 (C5 chunks)
-  a.group_v = (a.n_tt >= 64 || (a.n_tt >= 32 && pl.n_vt_fwd >= 1024)) ? 4 : 8;
+  a.group_v = (a.n_tt >= 64 || (a.n_tt >= 32 && pl.n_vt_fwd >= 512)) ? 4 : 8;
   a.n_vt = pl.n_vt_fwd;
   a.partials = partials;
   a.lslab = lslab;
