@@ -503,9 +503,13 @@ __device__ __forceinline__ int run_draw(const float (&kw)[RUN], float target) {
 // three probes, three independent reductions. The probed sets are nested and
 // summed in the same order, so the computed masses are ordered like the exact
 // ones and the decisions are consistent. Theta is a list value: once a single
-// entry remains in [lo, hi), it is theta.
+// entry remains in [lo, hi), it is theta. Once at most 64 entries remain in
+// the bracket, the mass at or above hi is fixed (B) and those entries move to
+// one per lane (through `scr`, 64 floats of LDS the list wave owns): each
+// later probe is B plus one compare per lane instead of a pass over the run.
 template <int RUN>
-__device__ __forceinline__ float list_theta(const float (&w)[RUN], float c, float P) {
+__device__ __forceinline__ float list_theta(const float (&w)[RUN], float c, float P, float* scr) {
+  const int lane = threadIdx.x & 63;
   // invariant: S(lo) >= P > S(hi); lo, hi and the decisions are wave-uniform
   uint32_t lo = __float_as_uint(c), hi = 0x3f800001u;  // nothing is above 1
   while (hi - lo > 1) {
@@ -524,6 +528,7 @@ __device__ __forceinline__ float list_theta(const float (&w)[RUN], float c, floa
           float, __builtin_amdgcn_readlane(__float_as_int(last), __builtin_ctzll(any)));
       return v;
     }
+    if (RUN > 1 && wave_sum(inside) <= 64) break;
     if (hi - lo > 3) {
       const uint32_t st = (hi - lo) >> 2;
       const uint32_t m1 = lo + st, m2 = m1 + st, m3 = m2 + st;
@@ -560,18 +565,69 @@ __device__ __forceinline__ float list_theta(const float (&w)[RUN], float c, floa
         hi = mid;
     }
   }
+  if (hi - lo <= 1) return __uint_as_float(lo);
+  // at most 64 entries in [lo, hi): B = the mass at or above hi, and the
+  // bracket's entries one per lane (in run order)
+  float base = 0.f;
+  int cnt = 0;
+#pragma unroll
+  for (int q = 0; q < RUN; ++q) {
+    const uint32_t b = __float_as_uint(w[q]);
+    base += b >= hi ? w[q] : 0.f;
+    cnt += (b >= lo && b < hi) ? 1 : 0;
+  }
+  const float B = wave_sum(base);
+  const int incl = wave_incl_scan(cnt);
+  const int n2 = __builtin_amdgcn_readlane(incl, 63);
+  int pos = incl - cnt;
+#pragma unroll
+  for (int q = 0; q < RUN; ++q) {
+    const uint32_t b = __float_as_uint(w[q]);
+    if (b >= lo && b < hi) scr[pos++] = w[q];
+  }
+  const float x = lane < n2 ? scr[lane] : 0.f;
+  const uint32_t bx = __float_as_uint(x);
+  while (hi - lo > 1) {
+    const unsigned long long in = __ballot(lane < n2 && bx >= lo && bx < hi);
+    if (__builtin_popcountll(in) == 1)
+      return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__float_as_int(x), __builtin_ctzll(in)));
+    if (hi - lo > 3) {
+      const uint32_t st = (hi - lo) >> 2;
+      const uint32_t m1 = lo + st, m2 = m1 + st, m3 = m2 + st;
+      const int g1 = __builtin_amdgcn_readfirstlane(B + wave_sum(bx >= m1 ? x : 0.f) >= P ? 1 : 0);
+      const int g2 = __builtin_amdgcn_readfirstlane(B + wave_sum(bx >= m2 ? x : 0.f) >= P ? 1 : 0);
+      const int g3 = __builtin_amdgcn_readfirstlane(B + wave_sum(bx >= m3 ? x : 0.f) >= P ? 1 : 0);
+      if (g3) {
+        lo = m3;
+      } else if (g2) {
+        lo = m2;
+        hi = m3;
+      } else if (g1) {
+        lo = m1;
+        hi = m2;
+      } else {
+        hi = m1;
+      }
+    } else {
+      const uint32_t mid = lo + (hi - lo) / 2;
+      if (__builtin_amdgcn_readfirstlane(B + wave_sum(bx >= mid ? x : 0.f) >= P ? 1 : 0))
+        lo = mid;
+      else
+        hi = mid;
+    }
+  }
   return __uint_as_float(lo);
 }
 
 // Completes a row's distribution from its final list (list wave): theta, the
 // tie cut and the kept mass. `kw` receives the kept weights of the lane's run.
 template <int RUN>
-__device__ __forceinline__ void run_dist(const RowShared& sh, int n, float c, float P, int V,
+__device__ __forceinline__ void run_dist(RowShared& sh, int n, float c, float P, int V,
                                          RowDist& d, float (&kw)[RUN]) {
   const int lane = threadIdx.x & 63;
   float w[RUN];
   load_run<RUN>(sh, n, w);
-  const float th = list_theta<RUN>(w, c, P);
+  const float th = list_theta<RUN>(w, c, P, sh.bw);  // the first list is spent by now
   d.theta = th;
   float above = 0.f;
   int ties = 0;
