@@ -1179,14 +1179,16 @@ mls_status mls_head_logits(int64_t T, int64_t V, int64_t d, int32_t dtype, const
   a.o = o;
   a.W = W;
   a.logits = logits;
+  const bool wide = dtype == MLS_BF16 && d % 64 == 0;
   a.n_tt = (int)((T + head_tile() - 1) / head_tile());
-  a.n_vt = (int)((V + head_tile() - 1) / head_tile());
+  const int rows = wide ? head_tile_rows(true, a.n_tt) : 128;
+  a.n_vt = (int)((V + rows - 1) / rows);
   a.group_v = 8;
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e;
   {
     ProfScope ps("head_logits", st);
-    e = launch_head_logits(a, dtype == MLS_F32, dtype == MLS_BF16 && d % 64 == 0, st);
+    e = launch_head_logits(a, dtype == MLS_F32, wide, rows, st);
   }
   if (e != hipSuccess) return hip_fail(e, "head logits launch");
   return MLS_OK;

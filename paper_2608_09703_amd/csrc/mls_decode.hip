@@ -4,9 +4,10 @@
 // 0.4, a smaller sub-model drafting gamma tokens and a larger one verifying).
 //
 // 1. head_logits_kernel: logits[t][v] = sum_k o[t][k] W[v][k] in fp32, on the
-//    MFMA tile core; the 128x128 fp32 tile is staged in LDS and leaves the
-//    block as 16-byte stores of token-major rows. Decode batches are small, so
-//    the [rows, V] logits are cheap next to the head itself.
+//    MFMA tile core (128 or 192 vocabulary rows x 128 tokens); the fp32 tile is
+//    staged in LDS and leaves the block as 16-byte stores of token-major rows.
+//    Decode batches are small, so the [rows, V] logits are cheap next to the
+//    head itself.
 // 2. sample_kernel: one 1024-thread block per row. The row's sampling
 //    distribution is softmax(l / temperature) restricted to the nucleus: the
 //    most probable tokens (ties: lower index first) up to and including the
@@ -46,9 +47,14 @@ __global__ __launch_bounds__(Mma::NT, 2) void head_logits_kernel(HeadArgs a) {
   constexpr int FM = Mma::FM;
   constexpr int FN = Mma::FN;
   constexpr int NT = Mma::NT;
-  constexpr int kChunks = BM / 4;  // 16-byte chunks (4 floats) per token row of the tile
-  static_assert(BN * BM * 4 <= Mma::kSmemBytes, "fp32 tile fits in the stage memory");
-  static_assert(kChunks == 32, "swizzle assumes 32 chunks per row");
+  constexpr int kChunks = BM / 4;          // 16-byte chunks (4 floats) per token row of the tile
+  constexpr int kSw = kChunks & -kChunks;  // chunk swizzle span: XOR stays inside aligned groups
+  // the fp32 tile leaves in one pass, or in one pass per wave column when it
+  // is larger than the stage memory
+  constexpr int kPasses = (BN * BM * 4 + Mma::kSmemBytes - 1) / Mma::kSmemBytes;
+  constexpr int kTok = BN / kPasses;  // tokens per pass
+  static_assert(kPasses == 1 || kPasses == Mma::kWGN, "one pass, or one per wave column");
+  static_assert(kTok * BM * 4 <= Mma::kSmemBytes, "a pass fits in the stage memory");
   __shared__ __attribute__((aligned(16))) char smem[Mma::kSmemBytes];
 
   const int tid = threadIdx.x;
@@ -67,36 +73,43 @@ __global__ __launch_bounds__(Mma::NT, 2) void head_logits_kernel(HeadArgs a) {
   mma.run(static_cast<const char*>(a.W), kb, vbase, a.V, static_cast<const char*>(a.o), kb, tbase,
           a.T, kb, smem, tid);
 
-  // stage: token row t holds 32 chunks of 4 vocabulary entries, chunk c at c ^ (t & 31)
+  // stage: token row t of a pass holds kChunks chunks of 4 vocabulary entries,
+  // chunk c at c ^ (t % kSw)
   float* st = reinterpret_cast<float*>(smem);
-#pragma unroll
-  for (int fn = 0; fn < FN; ++fn) {
-    const int t = Mma::col_of(wn, fn, lane);
-#pragma unroll
-    for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-      for (int rg = 0; rg < 4; ++rg) {
-        const int v0 = Mma::row_of(wm, fm, rg * 4, lane);  // multiple of 4
-        const float4 w = make_float4(mma.acc[fm][fn][rg * 4], mma.acc[fm][fn][rg * 4 + 1],
-                                     mma.acc[fm][fn][rg * 4 + 2], mma.acc[fm][fn][rg * 4 + 3]);
-        *reinterpret_cast<float4*>(st + t * BM + (((v0 >> 2) ^ (t & 31)) << 2)) = w;
-      }
-  }
-  __syncthreads();
   const bool vec = (a.V & 3) == 0;
-  for (int idx = tid; idx < BN * kChunks; idx += NT) {
-    const int t = idx / kChunks;
-    const int c = idx % kChunks;
-    const int64_t tg = tbase + t;
-    const int64_t v = vbase + 4 * c;
-    if (tg >= a.T || v >= a.V) continue;
-    const float4 w = *reinterpret_cast<const float4*>(st + t * BM + ((c ^ (t & 31)) << 2));
-    float* out = a.logits + tg * a.V + v;
-    if (vec) {
-      *reinterpret_cast<float4*>(out) = w;
-    } else {
-      const float x[4] = {w.x, w.y, w.z, w.w};
-      for (int q = 0; q < 4 && v + q < a.V; ++q) out[q] = x[q];
+#pragma unroll
+  for (int ps = 0; ps < kPasses; ++ps) {
+    if (ps > 0) __syncthreads();  // every read of the previous pass is done
+    if (kPasses == 1 || wn == ps) {
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) {
+        const int t = Mma::col_of(wn, fn, lane) - ps * kTok;
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+          for (int rg = 0; rg < 4; ++rg) {
+            const int v0 = Mma::row_of(wm, fm, rg * 4, lane);  // multiple of 4
+            const float4 w = make_float4(mma.acc[fm][fn][rg * 4], mma.acc[fm][fn][rg * 4 + 1],
+                                         mma.acc[fm][fn][rg * 4 + 2], mma.acc[fm][fn][rg * 4 + 3]);
+            *reinterpret_cast<float4*>(st + t * BM + (((v0 >> 2) ^ (t & (kSw - 1))) << 2)) = w;
+          }
+      }
+    }
+    __syncthreads();
+    for (int idx = tid; idx < kTok * kChunks; idx += NT) {
+      const int t = idx / kChunks;
+      const int c = idx % kChunks;
+      const int64_t tg = tbase + ps * kTok + t;
+      const int64_t v = vbase + 4 * c;
+      if (tg >= a.T || v >= a.V) continue;
+      const float4 w = *reinterpret_cast<const float4*>(st + t * BM + ((c ^ (t & (kSw - 1))) << 2));
+      float* out = a.logits + tg * a.V + v;
+      if (vec) {
+        *reinterpret_cast<float4*>(out) = w;
+      } else {
+        const float x[4] = {w.x, w.y, w.z, w.w};
+        for (int q = 0; q < 4 && v + q < a.V; ++q) out[q] = x[q];
+      }
     }
   }
 }
@@ -1115,23 +1128,35 @@ __global__ __launch_bounds__(kRowThreads) void verify_kernel(VerifyArgs a) {
 }
 
 using HeadWide = WideMma<128, 128, 2, 2, 2>;
+// 192 vocabulary rows: 80 KB of stages, two blocks fill a CU's LDS
+using HeadWide192 = WideMma<192, 128, 2, 2, 2>;
 using HeadGenBf16 = TileMma<Bf16, 128, 128, 2, 2>;
 using HeadGenF32 = TileMma<F32, 128, 128, 2, 2>;
 
 }  // namespace
 
 int head_tile() { return 128; }
+// Vocabulary rows of a head tile. With at least four token tiles (the
+// verifier's rows) the 192-row tile on the wide path: at 102 x 7 rows and
+// V = 49,152 it makes 1,536 blocks, three full rounds of two blocks per CU,
+// where 128-row tiles make 2,304 (four and a half).
+int head_tile_rows(bool wide, int n_tt) { return wide && n_tt >= 4 ? 192 : 128; }
 int row_elems_per_thread(int64_t V) {
   for (int e : {16, 32, 48, 64})
     if (V <= (int64_t)e * kRowThreads) return e;
   return 0;
 }
 
-hipError_t launch_head_logits(const HeadArgs& a, bool f32, bool wide, hipStream_t stream) {
+hipError_t launch_head_logits(const HeadArgs& a, bool f32, bool wide, int rows,
+                              hipStream_t stream) {
   const dim3 grid((unsigned)a.n_tt * (unsigned)a.n_vt);
+  if (rows != (f32 || !wide ? 128 : head_tile_rows(wide, a.n_tt))) return hipErrorInvalidValue;
   if (f32)
     hipLaunchKernelGGL((head_logits_kernel<HeadGenF32, F32>), grid, dim3(HeadGenF32::NT), 0, stream,
                        a);
+  else if (wide && rows == 192)
+    hipLaunchKernelGGL((head_logits_kernel<HeadWide192, Bf16>), grid, dim3(HeadWide192::NT), 0,
+                       stream, a);
   else if (wide)
     hipLaunchKernelGGL((head_logits_kernel<HeadWide, Bf16>), grid, dim3(HeadWide::NT), 0, stream, a);
   else

@@ -322,9 +322,12 @@ bool junction_shape(int64_t width, int* tpr, int* cpl);
 int64_t junction_max_width();
 hipError_t launch_junction_fwd(const JunctionArgs& a, bool act_f32, hipStream_t stream);
 hipError_t launch_junction_bwd(const JunctionArgs& a, bool act_f32, bool grad_f32, hipStream_t stream);
-int head_tile();
+int head_tile();  // token rows of a head tile
+int head_tile_rows(bool wide, int n_tt);  // vocabulary rows of a head tile (128 or 192)
 int row_elems_per_thread(int64_t V);
-hipError_t launch_head_logits(const HeadArgs& a, bool f32, bool wide, hipStream_t stream);
+// rows: head_tile_rows(wide, a.n_tt) on the wide bf16 path, else 128 (checked)
+hipError_t launch_head_logits(const HeadArgs& a, bool f32, bool wide, int rows,
+                              hipStream_t stream);
 hipError_t launch_sample(const SampleArgs& a, int ept, hipStream_t stream);
 hipError_t launch_row_params(const RowParamArgs& a, int ept, hipStream_t stream);
 hipError_t launch_verify(const VerifyArgs& a, int ept, hipStream_t stream);

@@ -41,6 +41,7 @@ HEAD = [
     (102, 1000, 1024, torch.bfloat16),   # wide bf16 core, one token tile
     (714, 777, 4352, torch.bfloat16),    # ragged V (scalar stores), several token tiles
     (600, 5000, 1024, torch.bfloat16),   # many rows: ragged token and vocabulary tiles, float4 stores
+    (512, 3840, 512, torch.bfloat16),    # four token tiles exactly, 192-row vocabulary tiles exactly
     (5, 49152, 1024, torch.bfloat16),    # full vocabulary, tiny batch
     (130, 513, 1000, torch.bfloat16),    # general bf16 core (d not a multiple of 64)
     (33, 300, 100, torch.float32),       # fp32 core
