@@ -192,3 +192,53 @@ def test_fused_full_size_sampled_rows(name):
         ign = yn == -100
         if ign.any():
             assert np.all(gpu["grad_h"][i][ign] == 0)
+
+
+def test_fused_five_chunks_match_the_recompute_plan_at_c5():
+    """At the C5 shape the stored-logit plan runs in five token chunks (its slab
+    budget), so grad_W is accumulated over five GEMM launches, a path no smaller
+    case reaches. Its gradients must equal the recompute plan's within the
+    gradient tolerance: two GPU paths that share no backward kernel, each
+    checked against the oracle at reduced T. Compared on the device, per
+    tensor and per row."""
+    from paper_2608_09703_amd import api as D
+    wl = WL.WORKLOADS["c5_m3_v262k_long"]
+    print(f"[fused-c5] M={wl.M} T={wl.T} V={wl.V} dims={wl.dims}", flush=True)
+    h, W, y = WL.make_inputs(wl, device=DEV)
+    g_ce, g_kl = oracle.coeffs(wl.M, -1, alpha=wl.alpha, tau=wl.tau)
+    gce = torch.tensor(g_ce, dtype=torch.float32, device=DEV)
+    gkl = torch.tensor(g_kl, dtype=torch.float32, device=DEV)
+    st = torch.cuda.current_stream(DEV).cuda_stream
+
+    p = D.make_problem(h, W, y, tau=wl.tau)
+    buf = D.Buffers(p, DEV)
+    ws_b = B.query_fwd_bwd_workspace(p)
+    ws = torch.empty(ws_b, dtype=torch.uint8, device=DEV)
+    gh_f = [torch.empty(x.shape, dtype=torch.float32, device=DEV) for x in h]
+    gW_f = [torch.empty(x.shape, dtype=torch.float32, device=DEV) for x in W]
+    B.distill_fwd_bwd(p, buf.stats.data_ptr(), buf.ce.data_ptr(), buf.kl.data_ptr(),
+                      buf.entropy.data_ptr(), gce.data_ptr(), gkl.data_ptr(),
+                      [x.data_ptr() for x in gh_f], [x.data_ptr() for x in gW_f], ws.data_ptr(),
+                      ws_b, st)
+    torch.cuda.synchronize()
+    del ws, buf
+
+    p2 = D.make_problem(h, W, y, tau=wl.tau)
+    buf2 = D.Buffers(p2, DEV)
+    D.forward(p2, buf2, DEV)
+    gh_r = [torch.empty(x.shape, dtype=torch.float32, device=DEV) for x in h]
+    gW_r = [torch.empty(x.shape, dtype=torch.float32, device=DEV) for x in W]
+    D.backward(p2, buf2, DEV, gce, gkl, gh_r, gW_r)
+    torch.cuda.synchronize()
+    del buf2
+
+    for i in range(wl.M):
+        for what, a, b in (("grad_h", gh_f[i], gh_r[i]), ("grad_W", gW_f[i], gW_r[i])):
+            a64, b64 = a.double(), b.double()
+            tensor = float(torch.linalg.norm(a64 - b64) / torch.linalg.norm(b64))
+            rows = torch.linalg.norm(a64 - b64, dim=1) / torch.linalg.norm(b64, dim=1).clamp_min(1e-30)
+            worst = float(rows.max())
+            print(f"  sub-model {i} {what}: rel {tensor:.2e}, worst row {worst:.2e}", flush=True)
+            assert tensor < 1e-2, (i, what, tensor)
+            assert worst < 5e-2, (i, what, worst)
+            del a64, b64, rows
