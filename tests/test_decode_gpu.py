@@ -243,12 +243,13 @@ def test_verify_rejection_draws_from_the_residual():
     np.testing.assert_allclose(freq, 1 / 3, atol=0.02)
 
 
-def test_full_size_step():
-    """The 500M-draft / 3B-verifier step at batch 102 and the paper's vocabulary.
-    The head kernel is checked on sampled rows; sampling and verification are
-    then checked on reference logits (fp32 torch products, not the HIP head),
-    which both sides take as input."""
-    wl = WL.DECODE["spec_500m_3b"]
+@pytest.mark.parametrize("name", ["spec_500m_3b", "spec_vanilla_b64"])
+def test_full_size_step(name):
+    """The 500M-draft / 3B-verifier step at the paper's vocabulary, batch 102
+    (the benchmark) and 64. The head kernel is checked on sampled rows;
+    sampling and verification are then checked on reference logits (fp32 torch
+    products, not the HIP head), which both sides take as input."""
+    wl = WL.DECODE[name]
     print(f"[decode] full-size step B={wl.batch} gamma={wl.gamma} V={wl.V}", flush=True)
     x = WL.make_decode_inputs(wl, device=DEV)
     B, G, V = wl.batch, wl.gamma, wl.V
