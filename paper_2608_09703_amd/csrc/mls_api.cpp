@@ -321,7 +321,7 @@ void fill_common(const mls_problem* p, const Plan& pl, FusedArgs& a) {
   a.inv_tau = 1.0f / p->tau;
   a.wide = pl.wide ? 1 : 0;
   // vocabulary tiles per group of the tile order: measured best at 8 for
-  // T <= 4096 and at 4 from T = 8192 on (C3-C5 shapes)
+  // T <= 4096 and at 4 from T = 8192 on (V = 128,256 and 262,144 shapes)
   a.group_v = pl.n_tt >= 64 ? 4 : 8;
   a.n_tt = pl.n_tt;
   a.T_pad = pl.T_pad;
@@ -394,9 +394,11 @@ hipError_t forward_chunk(const mls_problem* p, const Plan& pl, int64_t t0, int64
   a.T = tc;
   a.n_tt = (int)((tc + kFusedBN - 1) / kFusedBN);
   // vocabulary tiles per group of the tile order, measured per token chunk:
-  // 8 at 16 token tiles (C2 chunks; 4 and 16 are 5 % slower), 4 at 32 token
-  // tiles over 1002 vocabulary tiles (C3 chunks, 5 % faster than 8) and at 64
-  // (C4 chunks, 1 %), level at 52 over 2048 (C5 chunks)
+  // 8 at 16 token tiles over 393 vocabulary tiles (2,048-token chunks at
+  // V = 50,304; 4 and 16 are 5 % slower), 4 at 32 token tiles over 1,002
+  // vocabulary tiles (4,096-token chunks at V = 128,256; 5 % faster than 8)
+  // and at 64 (8,192-token chunks, 1 %), level at 52 over 2,048 (6,656-token
+  // chunks at V = 262,144)
   a.group_v = (a.n_tt >= 64 || (a.n_tt >= 32 && pl.n_vt_fwd >= 512)) ? 4 : 8;
   a.n_vt = pl.n_vt_fwd;
   a.partials = partials;

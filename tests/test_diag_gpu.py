@@ -194,7 +194,7 @@ def test_bitwise_deterministic():
         assert np.array_equal(x, z)
 
 
-FULL = ["c2_m3_v50k", "c4_m4_v128k_peaky", "c5_m3_v262k_long"]  # C5: records past 4 GiB
+FULL = ["c2_m3_v50k", "c4_m4_v128k_peaky", "c5_m3_v262k_long"]  # the last: records past 4 GiB
 
 
 @pytest.mark.parametrize("name", FULL)

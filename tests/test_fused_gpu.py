@@ -195,7 +195,7 @@ def test_fused_full_size_sampled_rows(name):
 
 
 def test_fused_five_chunks_match_the_recompute_plan_at_c5():
-    """At the C5 shape the stored-logit plan runs in five token chunks (its slab
+    """At T = 32,768, V = 262,144 the stored-logit plan runs in five token chunks (its slab
     budget), so grad_W is accumulated over five GEMM launches, a path no smaller
     case reaches. Its gradients must equal the recompute plan's within the
     gradient tolerance: two GPU paths that share no backward kernel, each

@@ -10,7 +10,8 @@ of the forward is a copy and must be bit-exact.
 
 Small cases cover every threads-per-row / chunks-per-lane shape, partial
 chunks, ragged T, both channel orders, every dtype pair, accumulation and
-zero-norm rows; the full-size C5 and paper-shape junctions are checked on
+zero-norm rows; the full-size junctions (T = 32,768, widths 1,536 / 3,072 /
+4,608, and the paper's 3B-suite widths) are checked on
 sampled rows (rows are independent).
 """
 
