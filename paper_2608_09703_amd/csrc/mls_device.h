@@ -201,6 +201,17 @@ __device__ __forceinline__ float shfl_xor32(float v) { return __shfl_xor(v, 32, 
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// 16-byte accesses with the non-temporal ("nt") cache policy, for streaming
+// passes that read or write each byte once.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load16_nt(const void* p) {
+  const u32x4_t v = __builtin_nontemporal_load(static_cast<const u32x4_t*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void store16_nt(void* p, uint4 v) {
+  __builtin_nontemporal_store(u32x4_t{v.x, v.y, v.z, v.w}, static_cast<u32x4_t*>(p));
+}
+
 template <typename E>
 __device__ __forceinline__ typename E::storage to_storage(float x);
 template <>

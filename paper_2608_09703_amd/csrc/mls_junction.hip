@@ -23,9 +23,24 @@ namespace {
 
 constexpr int kJBlock = 256;
 
-// 8 consecutive elements <-> 8 floats
+// 8 consecutive elements <-> 8 floats, through 16-byte accesses; NT: with the
+// non-temporal cache policy (the forward streams each byte once: 0.179 ->
+// 0.165 ms per step of both junctions at T = 32768 and widths 1536 / 3072 /
+// 4608; the backward ran 2 % slower with it)
+template <bool NT>
+__device__ __forceinline__ uint4 ld16(const void* p) {
+  return NT ? load16_nt(p) : *reinterpret_cast<const uint4*>(p);
+}
+template <bool NT>
+__device__ __forceinline__ void st16(void* p, uint4 v) {
+  if (NT)
+    store16_nt(p, v);
+  else
+    *reinterpret_cast<uint4*>(p) = v;
+}
+template <bool NT = false>
 __device__ __forceinline__ void load8(const uint16_t* p, float* v) {
-  const uint4 r = *reinterpret_cast<const uint4*>(p);
+  const uint4 r = ld16<NT>(p);
   const uint32_t w[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -33,23 +48,30 @@ __device__ __forceinline__ void load8(const uint16_t* p, float* v) {
     v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
   }
 }
+template <bool NT = false>
 __device__ __forceinline__ void load8(const float* p, float* v) {
-  const float4 a = reinterpret_cast<const float4*>(p)[0];
-  const float4 b = reinterpret_cast<const float4*>(p)[1];
-  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  const uint4 a = ld16<NT>(p);
+  const uint4 b = ld16<NT>(p + 4);
+  v[0] = __uint_as_float(a.x); v[1] = __uint_as_float(a.y);
+  v[2] = __uint_as_float(a.z); v[3] = __uint_as_float(a.w);
+  v[4] = __uint_as_float(b.x); v[5] = __uint_as_float(b.y);
+  v[6] = __uint_as_float(b.z); v[7] = __uint_as_float(b.w);
 }
+template <bool NT = false>
 __device__ __forceinline__ void store8(uint16_t* p, const float* v) {
   uint4 r;
   r.x = (uint32_t)to_storage<Bf16>(v[0]) | ((uint32_t)to_storage<Bf16>(v[1]) << 16);
   r.y = (uint32_t)to_storage<Bf16>(v[2]) | ((uint32_t)to_storage<Bf16>(v[3]) << 16);
   r.z = (uint32_t)to_storage<Bf16>(v[4]) | ((uint32_t)to_storage<Bf16>(v[5]) << 16);
   r.w = (uint32_t)to_storage<Bf16>(v[6]) | ((uint32_t)to_storage<Bf16>(v[7]) << 16);
-  *reinterpret_cast<uint4*>(p) = r;
+  st16<NT>(p, r);
 }
+template <bool NT = false>
 __device__ __forceinline__ void store8(float* p, const float* v) {
-  reinterpret_cast<float4*>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
-  reinterpret_cast<float4*>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
+  st16<NT>(p, make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
+                         __float_as_uint(v[3])));
+  st16<NT>(p + 4, make_uint4(__float_as_uint(v[4]), __float_as_uint(v[5]), __float_as_uint(v[6]),
+                             __float_as_uint(v[7])));
 }
 
 template <typename T>
@@ -104,12 +126,12 @@ __global__ __launch_bounds__(kJBlock) void junction_fwd_kernel(JunctionArgs a) {
   for (int c = 0; c < CPL; ++c) {
     const int64_t k = ((int64_t)c * TPR + j) * 8;
     if (live && k < dp) {
-      load8(o + k, ov[c]);
+      load8<true>(o + k, ov[c]);
 #pragma unroll
       for (int i = 0; i < 8; ++i) s[0] = fmaf(ov[c][i], ov[c][i], s[0]);
     }
     if (live && k < df) {
-      load8(e + k, ev[c]);
+      load8<true>(e + k, ev[c]);
 #pragma unroll
       for (int i = 0; i < 8; ++i) s[1] = fmaf(ev[c][i], ev[c][i], s[1]);
     }
@@ -126,9 +148,9 @@ __global__ __launch_bounds__(kJBlock) void junction_fwd_kernel(JunctionArgs a) {
     if (k < dp) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) ov[c][i] *= scale;
-      store8(xp + k, ov[c]);
+      store8<true>(xp + k, ov[c]);
     }
-    if (k < df) store8(xf + k, ev[c]);
+    if (k < df) store8<true>(xf + k, ev[c]);
   }
 }
 
