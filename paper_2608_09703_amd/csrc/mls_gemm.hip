@@ -87,6 +87,12 @@ using WideGemmW = WideMma<kWideBM, kWideBN, 2, 4, 2, 128, kLayoutMC, kLayoutMC, 
 // every element gets its own vector offset, which the descriptor checks. Each
 // kind of load is one loop with no branch inside, so a wave's loads are all in
 // flight together.
+// Cache policy of the fp32 output stores: non-temporal ("nt"). With it the
+// headline step's GEMMs and the forward that follows them ran 0.01-0.02 ms
+// faster each (7.76 -> 7.71 ms per step together with the forward's
+// non-temporal slab stores).
+constexpr int kStoreNT = 2;
+
 template <class Mma, bool INSIDE>
 struct TileIo {
   static constexpr int FM = Mma::FM;
@@ -189,7 +195,8 @@ struct TileIo {
 #pragma unroll
           for (int r = 0; r < 16; ++r)
             __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[fm][fn][r]), rc,
-                                                  voff(coff, ldc, fm, fn, r, 4), soff(ldc, fm, r, 4), 0);
+                                                  voff(coff, ldc, fm, fn, r, 4), soff(ldc, fm, r, 4),
+                                                  kStoreNT);
         __builtin_amdgcn_sched_barrier(0);
       }
     }
