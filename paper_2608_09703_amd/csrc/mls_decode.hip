@@ -105,7 +105,10 @@ __global__ __launch_bounds__(Mma::NT, 2) void head_logits_kernel(HeadArgs a) {
       const float4 w = *reinterpret_cast<const float4*>(st + t * BM + ((c ^ (t & (kSw - 1))) << 2));
       float* out = a.logits + tg * a.V + v;
       if (vec) {
-        *reinterpret_cast<float4*>(out) = w;
+        // whole lines, non-temporal (decode step 0.74 -> 0.72 ms: draft heads
+        // 0.141 -> 0.126 ms, verifier head 3 % faster)
+        store16_nt(out, make_uint4(__float_as_uint(w.x), __float_as_uint(w.y), __float_as_uint(w.z),
+                                   __float_as_uint(w.w)));
       } else {
         const float x[4] = {w.x, w.y, w.z, w.w};
         for (int q = 0; q < 4 && v + q < a.V; ++q) out[q] = x[q];
