@@ -11,9 +11,11 @@
 //
 // Memory-bound: each operand is read once and each result written once.
 // TPR threads own one token row (TPR/64 waves); every lane holds CPL chunks
-// of 8 consecutive elements of each operand in registers, read with 16-byte
-// loads at consecutive addresses across the lanes. The row's dot products are
-// reduced in fp32 (wave shuffles, then LDS across the row's waves).
+// of 8 elements of each operand in registers: in the forward 8 consecutive
+// elements (16-byte bf16 accesses), in the backward two groups of 4
+// consecutive elements TPR groups apart, so that its fp32 accesses cover whole
+// 1 KB runs per wave instruction. The row's dot products are reduced in fp32
+// (wave shuffles, then LDS across the row's waves).
 #include "mls_device.h"
 #include "mls_launch.h"
 
@@ -23,10 +25,11 @@ namespace {
 
 constexpr int kJBlock = 256;
 
-// 8 consecutive elements <-> 8 floats, through 16-byte accesses; NT: with the
-// non-temporal cache policy (the forward streams each byte once: 0.179 ->
-// 0.165 ms per step of both junctions at T = 32768 and widths 1536 / 3072 /
-// 4608; the backward ran 2 % slower with it)
+// 8 consecutive elements <-> 8 floats, through 16-byte accesses, for the
+// forward's lane mapping; NT: with the non-temporal cache policy (the forward
+// streams each byte once: 0.179 -> 0.165 ms per step of both junctions at
+// T = 32768 and widths 1536 / 3072 / 4608; on the backward's 4-element groups
+// the same mapping for the forward took 0.181 ms)
 template <bool NT>
 __device__ __forceinline__ uint4 ld16(const void* p) {
   return NT ? load16_nt(p) : *reinterpret_cast<const uint4*>(p);
@@ -74,6 +77,67 @@ __device__ __forceinline__ void store8(float* p, const float* v) {
                              __float_as_uint(v[7])));
 }
 
+// 4 consecutive elements <-> 4 floats (8 bytes of bf16, 16 of fp32), for the
+// backward's lane mapping; NT: with the non-temporal cache policy
+typedef unsigned int u32x2j __attribute__((ext_vector_type(2)));
+template <bool NT>
+__device__ __forceinline__ uint2 ld8b(const void* p) {
+  if (NT) {
+    const u32x2j v = __builtin_nontemporal_load(static_cast<const u32x2j*>(p));
+    return make_uint2(v.x, v.y);
+  }
+  return *reinterpret_cast<const uint2*>(p);
+}
+template <bool NT>
+__device__ __forceinline__ void st8b(void* p, uint2 v) {
+  if (NT)
+    __builtin_nontemporal_store(u32x2j{v.x, v.y}, static_cast<u32x2j*>(p));
+  else
+    *reinterpret_cast<uint2*>(p) = v;
+}
+template <bool NT>
+__device__ __forceinline__ uint4 ld16b(const void* p) {
+  return NT ? load16_nt(p) : *reinterpret_cast<const uint4*>(p);
+}
+template <bool NT>
+__device__ __forceinline__ void st16b(void* p, uint4 v) {
+  if (NT)
+    store16_nt(p, v);
+  else
+    *reinterpret_cast<uint4*>(p) = v;
+}
+template <bool NT>
+__device__ __forceinline__ void load4(const uint16_t* p, float* v) {
+  const uint2 r = ld8b<NT>(p);
+  v[0] = __uint_as_float(r.x << 16);
+  v[1] = __uint_as_float(r.x & 0xffff0000u);
+  v[2] = __uint_as_float(r.y << 16);
+  v[3] = __uint_as_float(r.y & 0xffff0000u);
+}
+template <bool NT>
+__device__ __forceinline__ void load4(const float* p, float* v) {
+  const uint4 r = ld16b<NT>(p);
+  v[0] = __uint_as_float(r.x);
+  v[1] = __uint_as_float(r.y);
+  v[2] = __uint_as_float(r.z);
+  v[3] = __uint_as_float(r.w);
+}
+template <bool NT>
+__device__ __forceinline__ void store4(uint16_t* p, const float* v) {
+  st8b<NT>(p, make_uint2((uint32_t)to_storage<Bf16>(v[0]) | ((uint32_t)to_storage<Bf16>(v[1]) << 16),
+                         (uint32_t)to_storage<Bf16>(v[2]) | ((uint32_t)to_storage<Bf16>(v[3]) << 16)));
+}
+template <bool NT>
+__device__ __forceinline__ void store4(float* p, const float* v) {
+  st16b<NT>(p, make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
+                          __float_as_uint(v[3])));
+}
+
+// Cache policy of the backward: non-temporal (0.448 -> 0.413 ms per step of
+// both junctions at T = 32768, widths 1536 / 3072 / 4608, with its lane
+// mapping; with the forward's 8-element mapping it ran 2 % slower)
+constexpr bool kBwdNT = true;
+
 template <typename T>
 struct Elt;
 template <>
@@ -107,6 +171,13 @@ __device__ __forceinline__ void row_sums(float* v, float (*red)[NV]) {
     for (int w = 0; w < TPR / 64; ++w) s += red[first + w][q];
     v[q] = s;
   }
+}
+
+// Backward lane mapping: element offset of group g (0 or 1) of chunk c of
+// lane j; groups of 4 elements, 2 * CPL of them per lane, TPR groups apart.
+template <int TPR>
+__device__ __forceinline__ int64_t group_at(int c, int g, int j) {
+  return ((int64_t)(2 * c + g) * TPR + j) * 4;
 }
 
 template <typename A, int TPR, int CPL>
@@ -172,31 +243,35 @@ __global__ __launch_bounds__(kJBlock) void junction_bwd_kernel(JunctionArgs a) {
   float ov[CPL][8], gv[CPL][8];
   float s[3] = {0.f, 0.f, 0.f};  // ||o||^2, ||e||^2, g.o
 #pragma unroll
-  for (int c = 0; c < CPL; ++c) {
-    const int64_t k = ((int64_t)c * TPR + j) * 8;
-    if (live && k < dp) {
-      load8(o + k, ov[c]);
-      load8(gp + k, gv[c]);
+  for (int c = 0; c < CPL; ++c)
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        s[0] = fmaf(ov[c][i], ov[c][i], s[0]);
-        s[2] = fmaf(gv[c][i], ov[c][i], s[2]);
+    for (int g = 0; g < 2; ++g) {
+      const int64_t k = group_at<TPR>(c, g, j);
+      if (live && k < dp) {
+        load4<kBwdNT>(o + k, &ov[c][4 * g]);
+        load4<kBwdNT>(gp + k, &gv[c][4 * g]);
+#pragma unroll
+        for (int i = 4 * g; i < 4 * g + 4; ++i) {
+          s[0] = fmaf(ov[c][i], ov[c][i], s[0]);
+          s[2] = fmaf(gv[c][i], ov[c][i], s[2]);
+        }
       }
     }
-  }
   // the fresh block's gradient is loaded here too, so that it is in flight
   // while the row reduction runs
   float ev[CPL][8], gdv[CPL][8];
 #pragma unroll
-  for (int c = 0; c < CPL; ++c) {
-    const int64_t k = ((int64_t)c * TPR + j) * 8;
-    if (live && k < df) {
-      load8(e + k, ev[c]);
-      load8(gf + k, gdv[c]);
+  for (int c = 0; c < CPL; ++c)
 #pragma unroll
-      for (int i = 0; i < 8; ++i) s[1] = fmaf(ev[c][i], ev[c][i], s[1]);
+    for (int g = 0; g < 2; ++g) {
+      const int64_t k = group_at<TPR>(c, g, j);
+      if (live && k < df) {
+        load4<kBwdNT>(e + k, &ev[c][4 * g]);
+        load4<kBwdNT>(gf + k, &gdv[c][4 * g]);
+#pragma unroll
+        for (int i = 4 * g; i < 4 * g + 4; ++i) s[1] = fmaf(ev[c][i], ev[c][i], s[1]);
+      }
     }
-  }
   row_sums<TPR, 3>(s, red);
   if (!live) return;
   const bool ok = s[0] > 0.f && s[1] > 0.f;
@@ -207,30 +282,31 @@ __global__ __launch_bounds__(kJBlock) void junction_bwd_kernel(JunctionArgs a) {
   TG* go = static_cast<TG*>(a.g_o) + t * dp;
   TG* ge = static_cast<TG*>(a.g_e) + t * df;
 #pragma unroll
-  for (int c = 0; c < CPL; ++c) {
-    const int64_t k = ((int64_t)c * TPR + j) * 8;
-    if (k < dp) {
-      float out[8];
-      if (a.accumulate) load8(go + k, out);
+  for (int c = 0; c < CPL; ++c)
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const float v = sc * fmaf(-proj, ov[c][i], gv[c][i]);
-        out[i] = a.accumulate ? out[i] + v : v;
-      }
-      store8(go + k, out);
-    }
-    if (k < df) {
-      float out[8];
-      const float* gd = gdv[c];
-      if (a.accumulate) load8(ge + k, out);
+    for (int g = 0; g < 2; ++g) {
+      const int64_t k = group_at<TPR>(c, g, j);
+      if (k < dp) {
+        float out[4];
+        if (a.accumulate) load4<kBwdNT>(go + k, out);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const float v = fmaf(fe, ev[c][i], gd[i]);
-        out[i] = a.accumulate ? out[i] + v : v;
+        for (int i = 0; i < 4; ++i) {
+          const float v = sc * fmaf(-proj, ov[c][4 * g + i], gv[c][4 * g + i]);
+          out[i] = a.accumulate ? out[i] + v : v;
+        }
+        store4<kBwdNT>(go + k, out);
       }
-      store8(ge + k, out);
+      if (k < df) {
+        float out[4];
+        if (a.accumulate) load4<kBwdNT>(ge + k, out);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float v = fmaf(fe, ev[c][4 * g + i], gdv[c][4 * g + i]);
+          out[i] = a.accumulate ? out[i] + v : v;
+        }
+        store4<kBwdNT>(ge + k, out);
+      }
     }
-  }
 }
 
 template <typename A, int TPR>
