@@ -25,11 +25,29 @@ namespace {
 
 constexpr int kJBlock = 256;
 
-// 8 consecutive elements <-> 8 floats, through 16-byte accesses, for the
-// forward's lane mapping; NT: with the non-temporal cache policy (the forward
-// streams each byte once: 0.179 -> 0.165 ms per step of both junctions at
-// T = 32768 and widths 1536 / 3072 / 4608; on the backward's 4-element groups
-// the same mapping for the forward took 0.181 ms)
+// Cache policy of each pass (both junctions of T = 32768 tokens at widths
+// 1536 / 3072 / 4608, ms per step): non-temporal in the forward (0.179 ->
+// 0.165) and in the backward with its lane mapping (0.448 -> 0.413; with the
+// forward's mapping, 0.452 -> 0.462)
+constexpr bool kFwdNT = true;
+constexpr bool kBwdNT = true;
+
+typedef unsigned int u32x2j __attribute__((ext_vector_type(2)));
+template <bool NT>
+__device__ __forceinline__ uint2 ld8(const void* p) {
+  if (NT) {
+    const u32x2j v = __builtin_nontemporal_load(static_cast<const u32x2j*>(p));
+    return make_uint2(v.x, v.y);
+  }
+  return *reinterpret_cast<const uint2*>(p);
+}
+template <bool NT>
+__device__ __forceinline__ void st8(void* p, uint2 v) {
+  if (NT)
+    __builtin_nontemporal_store(u32x2j{v.x, v.y}, static_cast<u32x2j*>(p));
+  else
+    *reinterpret_cast<uint2*>(p) = v;
+}
 template <bool NT>
 __device__ __forceinline__ uint4 ld16(const void* p) {
   return NT ? load16_nt(p) : *reinterpret_cast<const uint4*>(p);
@@ -41,7 +59,10 @@ __device__ __forceinline__ void st16(void* p, uint4 v) {
   else
     *reinterpret_cast<uint4*>(p) = v;
 }
-template <bool NT = false>
+
+// 8 consecutive elements <-> 8 floats, 16-byte accesses (the forward's lane
+// mapping)
+template <bool NT>
 __device__ __forceinline__ void load8(const uint16_t* p, float* v) {
   const uint4 r = ld16<NT>(p);
   const uint32_t w[4] = {r.x, r.y, r.z, r.w};
@@ -51,7 +72,7 @@ __device__ __forceinline__ void load8(const uint16_t* p, float* v) {
     v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
   }
 }
-template <bool NT = false>
+template <bool NT>
 __device__ __forceinline__ void load8(const float* p, float* v) {
   const uint4 a = ld16<NT>(p);
   const uint4 b = ld16<NT>(p + 4);
@@ -60,7 +81,7 @@ __device__ __forceinline__ void load8(const float* p, float* v) {
   v[4] = __uint_as_float(b.x); v[5] = __uint_as_float(b.y);
   v[6] = __uint_as_float(b.z); v[7] = __uint_as_float(b.w);
 }
-template <bool NT = false>
+template <bool NT>
 __device__ __forceinline__ void store8(uint16_t* p, const float* v) {
   uint4 r;
   r.x = (uint32_t)to_storage<Bf16>(v[0]) | ((uint32_t)to_storage<Bf16>(v[1]) << 16);
@@ -69,7 +90,7 @@ __device__ __forceinline__ void store8(uint16_t* p, const float* v) {
   r.w = (uint32_t)to_storage<Bf16>(v[6]) | ((uint32_t)to_storage<Bf16>(v[7]) << 16);
   st16<NT>(p, r);
 }
-template <bool NT = false>
+template <bool NT>
 __device__ __forceinline__ void store8(float* p, const float* v) {
   st16<NT>(p, make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
                          __float_as_uint(v[3])));
@@ -77,38 +98,11 @@ __device__ __forceinline__ void store8(float* p, const float* v) {
                              __float_as_uint(v[7])));
 }
 
-// 4 consecutive elements <-> 4 floats (8 bytes of bf16, 16 of fp32), for the
-// backward's lane mapping; NT: with the non-temporal cache policy
-typedef unsigned int u32x2j __attribute__((ext_vector_type(2)));
-template <bool NT>
-__device__ __forceinline__ uint2 ld8b(const void* p) {
-  if (NT) {
-    const u32x2j v = __builtin_nontemporal_load(static_cast<const u32x2j*>(p));
-    return make_uint2(v.x, v.y);
-  }
-  return *reinterpret_cast<const uint2*>(p);
-}
-template <bool NT>
-__device__ __forceinline__ void st8b(void* p, uint2 v) {
-  if (NT)
-    __builtin_nontemporal_store(u32x2j{v.x, v.y}, static_cast<u32x2j*>(p));
-  else
-    *reinterpret_cast<uint2*>(p) = v;
-}
-template <bool NT>
-__device__ __forceinline__ uint4 ld16b(const void* p) {
-  return NT ? load16_nt(p) : *reinterpret_cast<const uint4*>(p);
-}
-template <bool NT>
-__device__ __forceinline__ void st16b(void* p, uint4 v) {
-  if (NT)
-    store16_nt(p, v);
-  else
-    *reinterpret_cast<uint4*>(p) = v;
-}
+// 4 consecutive elements <-> 4 floats, 8-byte (bf16) or 16-byte (fp32)
+// accesses (the backward's lane mapping)
 template <bool NT>
 __device__ __forceinline__ void load4(const uint16_t* p, float* v) {
-  const uint2 r = ld8b<NT>(p);
+  const uint2 r = ld8<NT>(p);
   v[0] = __uint_as_float(r.x << 16);
   v[1] = __uint_as_float(r.x & 0xffff0000u);
   v[2] = __uint_as_float(r.y << 16);
@@ -116,7 +110,7 @@ __device__ __forceinline__ void load4(const uint16_t* p, float* v) {
 }
 template <bool NT>
 __device__ __forceinline__ void load4(const float* p, float* v) {
-  const uint4 r = ld16b<NT>(p);
+  const uint4 r = ld16<NT>(p);
   v[0] = __uint_as_float(r.x);
   v[1] = __uint_as_float(r.y);
   v[2] = __uint_as_float(r.z);
@@ -124,19 +118,14 @@ __device__ __forceinline__ void load4(const float* p, float* v) {
 }
 template <bool NT>
 __device__ __forceinline__ void store4(uint16_t* p, const float* v) {
-  st8b<NT>(p, make_uint2((uint32_t)to_storage<Bf16>(v[0]) | ((uint32_t)to_storage<Bf16>(v[1]) << 16),
-                         (uint32_t)to_storage<Bf16>(v[2]) | ((uint32_t)to_storage<Bf16>(v[3]) << 16)));
+  st8<NT>(p, make_uint2((uint32_t)to_storage<Bf16>(v[0]) | ((uint32_t)to_storage<Bf16>(v[1]) << 16),
+                        (uint32_t)to_storage<Bf16>(v[2]) | ((uint32_t)to_storage<Bf16>(v[3]) << 16)));
 }
 template <bool NT>
 __device__ __forceinline__ void store4(float* p, const float* v) {
-  st16b<NT>(p, make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
-                          __float_as_uint(v[3])));
+  st16<NT>(p, make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
+                         __float_as_uint(v[3])));
 }
-
-// Cache policy of the backward: non-temporal (0.448 -> 0.413 ms per step of
-// both junctions at T = 32768, widths 1536 / 3072 / 4608, with its lane
-// mapping; with the forward's 8-element mapping it ran 2 % slower)
-constexpr bool kBwdNT = true;
 
 template <typename T>
 struct Elt;
@@ -197,12 +186,12 @@ __global__ __launch_bounds__(kJBlock) void junction_fwd_kernel(JunctionArgs a) {
   for (int c = 0; c < CPL; ++c) {
     const int64_t k = ((int64_t)c * TPR + j) * 8;
     if (live && k < dp) {
-      load8<true>(o + k, ov[c]);
+      load8<kFwdNT>(o + k, ov[c]);
 #pragma unroll
       for (int i = 0; i < 8; ++i) s[0] = fmaf(ov[c][i], ov[c][i], s[0]);
     }
     if (live && k < df) {
-      load8<true>(e + k, ev[c]);
+      load8<kFwdNT>(e + k, ev[c]);
 #pragma unroll
       for (int i = 0; i < 8; ++i) s[1] = fmaf(ev[c][i], ev[c][i], s[1]);
     }
@@ -219,9 +208,9 @@ __global__ __launch_bounds__(kJBlock) void junction_fwd_kernel(JunctionArgs a) {
     if (k < dp) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) ov[c][i] *= scale;
-      store8<true>(xp + k, ov[c]);
+      store8<kFwdNT>(xp + k, ov[c]);
     }
-    if (k < df) store8<true>(xf + k, ev[c]);
+    if (k < df) store8<kFwdNT>(xf + k, ev[c]);
   }
 }
 
