@@ -87,10 +87,12 @@ using WideGemmW = WideMma<kWideBM, kWideBN, 2, 4, 2, 128, kLayoutMC, kLayoutMC, 
 // every element gets its own vector offset, which the descriptor checks. Each
 // kind of load is one loop with no branch inside, so a wave's loads are all in
 // flight together.
-// Cache policy of the fp32 output stores: non-temporal ("nt"). With it the
-// headline step's GEMMs and the forward that follows them ran 0.01-0.02 ms
-// faster each (7.76 -> 7.71 ms per step together with the forward's
-// non-temporal slab stores).
+// Cache policy of the fp32 output stores and of the reads of an fp32 output
+// into the accumulators: non-temporal ("nt"), as each such element is touched
+// once per launch. With the stores the headline step's GEMMs and the forward
+// that follows them ran 0.01-0.02 ms faster each (7.76 -> 7.71 ms per step
+// together with the forward's non-temporal slab stores); the reads took the
+// GEMMs from 4.43-4.45 to 4.41-4.42 ms per step.
 constexpr int kStoreNT = 2;
 
 template <class Mma, bool INSIDE>
@@ -111,7 +113,8 @@ struct TileIo {
   __device__ __forceinline__ static float ld32(__amdgpu_buffer_rsrc_t rs, const uint32_t* coff,
                                                int ldc, int fm, int fn, int r) {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                                         rs, voff(coff, ldc, fm, fn, r, 4), soff(ldc, fm, r, 4), 0));
+                                         rs, voff(coff, ldc, fm, fn, r, 4), soff(ldc, fm, r, 4),
+                                         kStoreNT));
   }
   __device__ __forceinline__ static float ld16(__amdgpu_buffer_rsrc_t rs, const uint32_t* coff,
                                                int ldc, int fm, int fn, int r) {
