@@ -713,10 +713,10 @@ def main():
         "peak": peak / 1e12,
         "unit": "TFLOP/s",
         "frac": achieved / peak,
-        # the committed summaries profile the default plan (and the diagnostics);
-        # the other plans launch differently sized kernels
-        "traffic": (profiled_traffic(name, dom, args.diagnostics)
-                    if args.diagnostics or args.path == "fwd_bwd" else None),
+        # the recompute plan has a summary of its own (its launches differ from
+        # the default plan's); --path separate runs the same launches
+        "traffic": profiled_traffic(name, dom, args.diagnostics or
+                                    ("recompute" if args.path != "fwd_bwd" else False)),
     }
 
     if args.copy_mib > 0:
